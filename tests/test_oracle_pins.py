@@ -1,0 +1,295 @@
+"""Pins of the fp64 oracle against things other than itself.
+
+Each test checks the oracle against brute force on tiny inputs, a closed
+form, a textbook or library routine, or an invariant that follows from the
+paper's definitions (Sec. "Reuse-aware Expert Gating").  They are chosen so
+that a dropped term, a wrong sign or index, or a transposed operand in the
+oracle fails at least one of them.
+"""
+
+import itertools
+
+import numpy as np
+import pytest
+from scipy.special import expit, softmax
+
+import oracle
+from oracle import s2moe_oracle as O
+
+
+def _distinct(rng, shape, scale=1.0):
+    """Random values whose sums over small subsets are pairwise distinct."""
+    v = rng.standard_normal(shape) * scale
+    return v + rng.random(shape) * 1e-3
+
+
+def brute_topk(values, k):
+    """Best k-subset by total value (unique when values are generic)."""
+    best = max(itertools.combinations(range(len(values)), k),
+               key=lambda s: sum(values[i] for i in s))
+    return sorted(best)
+
+
+# ---------------------------------------------------------------- route (a1, a2)
+def test_router_one_hot_rows_pick_coordinates():
+    """W_r with unit rows e_{p(e)} gives ell_{b,e} = x_{b,p(e)}: pins the
+    orientation ell = W_r x (a transposed router changes which coordinate is
+    read)."""
+    rng = np.random.default_rng(0)
+    B, H, E = 5, 16, 6
+    x = rng.standard_normal((B, H)).astype(np.float32)
+    perm = np.array([3, 11, 0, 7, 15, 2])
+    W = np.zeros((E, H), np.float32)
+    W[np.arange(E), perm] = 1.0
+    r = oracle.route(x, W, 2, "f32")
+    np.testing.assert_array_equal(r["logits"], x[:, perm].astype(np.float64))
+
+
+def test_router_matches_explicit_loop_on_bf16_bits():
+    """Logits on bf16 inputs equal the dot products of the decoded values;
+    decoded values are checked against known bf16 encodings."""
+    known = {0x3F80: 1.0, 0xC000: -2.0, 0x3F81: 1.0078125, 0x0000: 0.0,
+             0x4049: 3.140625, 0xBF00: -0.5}
+    for bits, val in known.items():
+        assert oracle.upcast(np.array([bits], np.uint16), "bf16")[0] == val
+    x = np.array([[0x3F80, 0xC000, 0x4049]], np.uint16)     # [1, -2, 3.140625]
+    W = np.array([[0x3F80, 0x3F80, 0x0000],                 # [1, 1, 0]
+                  [0x0000, 0xBF00, 0x3F80]], np.uint16)     # [0, -0.5, 1]
+    r = oracle.route(x, W, 1, "bf16")
+    np.testing.assert_array_equal(r["logits"], [[-1.0, 1.0 + 3.140625]])
+
+
+@pytest.mark.parametrize("seed", range(20))
+def test_plain_topk_and_gap_bruteforce(seed):
+    rng = np.random.default_rng(seed)
+    E = int(rng.integers(3, 9))
+    k = int(rng.integers(1, min(4, E)))
+    B = int(rng.integers(1, 6))
+    H = 8
+    x = rng.standard_normal((B, H))
+    W = rng.standard_normal((E, H))
+    r = oracle.route(x.astype(np.float32), W.astype(np.float32), k, "f32")
+    for b in range(B):
+        ell = list(r["logits"][b])
+        assert list(r["plain_idx"][b]) == brute_topk(ell, k)
+        desc = sorted(ell, reverse=True)
+        assert r["gap"][b] == desc[0] - desc[k]          # top-1 minus (k+1)-th
+
+
+def test_ties_break_toward_lower_expert_index():
+    ell = np.array([[1.0, 2.0, 2.0, 0.5, 2.0]])
+    r_idx = O.top_k_ascending(ell[0], 2)
+    assert list(r_idx) == [1, 2]
+    assert list(O.rank_order(np.array([0.0, -0.0, 0.0]))) == [0, 1, 2]
+
+
+# ---------------------------------------------------------------- gating (a3-a5)
+def brute_gate(ell, w, k, cap, alpha):
+    """Independent gating by subset enumeration."""
+    B, E = ell.shape
+    g = [sum(max(w[b], 0.0) * ell[b][e] for b in range(B)) for e in range(E)]
+    pref = set(brute_topk(g, cap))
+    idx = []
+    for b in range(B):
+        desc = sorted(ell[b], reverse=True)
+        lam = alpha * (desc[0] - desc[k])
+        val = [ell[b][e] + (lam if e in pref else 0.0) for e in range(E)]
+        idx.append(brute_topk(val, k))
+    return pref, idx
+
+
+@pytest.mark.parametrize("seed", range(30))
+def test_reuse_gate_bruteforce(seed):
+    rng = np.random.default_rng(100 + seed)
+    E = int(rng.integers(4, 9))
+    k = int(rng.integers(1, min(3, E - 1) + 1))
+    cap = int(rng.integers(k, min(6, E) + 1))
+    B = int(rng.integers(1, 7))
+    alpha = float(rng.choice([0.0, 0.3, 0.5, 0.9, 2.0]))
+    ell = _distinct(rng, (B, E))
+    w = rng.random(B)
+    gap = np.array([sorted(row, reverse=True)[0] - sorted(row, reverse=True)[k] for row in ell])
+    plain = np.array([sorted(brute_topk(list(row), k)) for row in ell])
+    gt = oracle.reuse_gate(ell, gap, plain, w, k, cap, alpha)
+    pref, idx = brute_gate(ell, w, k, cap, alpha)
+    assert set(np.nonzero(gt["pref"])[0]) == pref
+    assert [list(r) for r in gt["idx"]] == idx
+    # g pinned by one-hot confidences: g = ell_b0
+    b0 = int(rng.integers(0, B))
+    onehot = np.zeros(B)
+    onehot[b0] = 0.7
+    g1 = oracle.reuse_gate(ell, gap, plain, onehot, k, cap, alpha)["g"]
+    np.testing.assert_allclose(g1, 0.7 * ell[b0], rtol=0, atol=1e-15)
+
+
+def test_bias_is_alpha_times_top1_minus_kplus1_gap():
+    """One token, E=5, k=2, E* forced to {3}.  Expert 3 enters the top-2 iff
+    ell_3 + alpha*gap > ell_(2).  With ell = [3, 2, 1.5, 1, 0]: gap = 3 - 1.5,
+    so expert 3 replaces expert 1 exactly when alpha > (2 - 1) / 1.5."""
+    ell = np.array([[3.0, 2.0, 1.5, 1.0, 0.0],
+                    [0.0, 0.0, 0.0, 50.0, 0.0]])   # token 1 pushes g_3 to the top
+    w = np.array([0.0, 1.0])
+    k, cap = 2, 2
+    gap = np.array([1.5, 50.0])
+    plain = np.array([[0, 1], [2, 3]])
+    a_star = 1.0 / 1.5
+    lo = oracle.reuse_gate(ell, gap, plain, w, k, cap, a_star - 1e-9)
+    hi = oracle.reuse_gate(ell, gap, plain, w, k, cap, a_star + 1e-9)
+    assert lo["pref"][3] == 1
+    assert list(lo["idx"][0]) == [0, 1]
+    assert list(hi["idx"][0]) == [0, 3]
+    np.testing.assert_allclose(hi["lam"][0], (a_star + 1e-9) * 1.5)
+    # absolute bias reading: lambda = alpha
+    ab = oracle.reuse_gate(ell, gap, plain, w, k, cap, 1.0 + 1e-9, oracle.BIAS_ABSOLUTE)
+    assert list(ab["idx"][0]) == [0, 3]
+    ab = oracle.reuse_gate(ell, gap, plain, w, k, cap, 1.0 - 1e-9, oracle.BIAS_ABSOLUTE)
+    assert list(ab["idx"][0]) == [0, 1]
+
+
+def test_gate_weights_are_softmax_of_original_logits():
+    rng = np.random.default_rng(7)
+    B, E, k, cap = 6, 8, 3, 5
+    ell = _distinct(rng, (B, E), 2.0)
+    w = rng.random(B)
+    gap = np.array([np.sort(r)[::-1][0] - np.sort(r)[::-1][k] for r in ell])
+    plain = np.array([O.top_k_ascending(r, k) for r in ell])
+    gt = oracle.reuse_gate(ell, gap, plain, w, k, cap, 0.8)
+    for b in range(B):
+        np.testing.assert_allclose(gt["gate_w"][b], softmax(ell[b, gt["idx"][b]]),
+                                   rtol=1e-14, atol=0)
+    gb = oracle.reuse_gate(ell, gap, plain, w, k, cap, 0.8, oracle.GATE_FROM_BIASED)
+    for b in range(B):
+        np.testing.assert_allclose(gb["gate_w"][b], softmax(gb["biased"][b, gb["idx"][b]]),
+                                   rtol=1e-14, atol=0)
+
+
+def test_bucketing_matches_stable_argsort():
+    rng = np.random.default_rng(3)
+    for _ in range(20):
+        E = int(rng.integers(2, 20))
+        k = int(rng.integers(1, min(E, 5)))
+        B = int(rng.integers(1, 40))
+        idx = np.array([np.sort(rng.choice(E, k, replace=False)) for _ in range(B)])
+        bk = oracle.bucket(idx, E)
+        flat = idx.reshape(-1)
+        np.testing.assert_array_equal(bk["slot"], np.argsort(flat, kind="stable"))
+        np.testing.assert_array_equal(bk["count"], np.bincount(flat, minlength=E))
+        np.testing.assert_array_equal(bk["offset"][1:], np.cumsum(np.bincount(flat, minlength=E)))
+        u = np.unique(flat)
+        assert bk["n_uniq"] == u.size
+        np.testing.assert_array_equal(bk["uniq"][:u.size], u)
+        assert np.all(bk["uniq"][u.size:] == -1)
+        assert bk["reuse_ratio"] == u.size / (B * k)
+
+
+# ---------------------------------------------------------------- FFN (a7-a11)
+def test_swiglu_closed_form_identity_weights():
+    """W_g = c I, W_u = I, W_d = P (a permutation): y = P (silu(c x) * x).
+    Swapping gate and up gives silu(x) * c x, a transposed W_d gives P^T."""
+    rng = np.random.default_rng(11)
+    H = 8
+    c = 1.75                       # exact in fp32
+    x = rng.standard_normal((3, H)).astype(np.float32)
+    P = np.eye(H)[[2, 5, 0, 7, 1, 3, 6, 4]]
+    experts = {"gate": (c * np.eye(H))[None].astype(np.float32),
+               "up": np.eye(H)[None].astype(np.float32),
+               "down": P[None].astype(np.float32)}
+    gt = {"idx": np.zeros((3, 1), np.int32)}
+    out = oracle.verify_moe(x, experts, {}, gt, 1, "f32", "f32")
+    xd = x.astype(np.float64)
+    expect = (c * xd * expit(c * xd) * xd) @ P.T
+    np.testing.assert_allclose(out, expect, rtol=1e-14, atol=1e-15)
+
+
+def test_down_projection_is_linear_and_zero_gives_zero():
+    rng = np.random.default_rng(12)
+    H, F, E = 8, 16, 3
+    x = rng.standard_normal((4, H)).astype(np.float32)
+    ex = {n: rng.standard_normal((E, F, H)).astype(np.float32) for n in ("gate", "up")}
+    ex["down"] = rng.standard_normal((E, H, F)).astype(np.float32)
+    gt = {"idx": np.array([[0, 2], [1, 2], [0, 1], [2, 0]], np.int32)}
+    base = oracle.verify_moe(x, ex, {}, gt, 2, "f32", "f32")
+    ex2 = dict(ex, down=ex["down"] * np.float32(2.0))
+    np.testing.assert_allclose(oracle.verify_moe(x, ex2, {}, gt, 2, "f32", "f32"), 2 * base,
+                               rtol=1e-14)
+    ex0 = dict(ex, down=np.zeros_like(ex["down"]))
+    assert not oracle.verify_moe(x, ex0, {}, gt, 2, "f32", "f32").any()
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_dense_then_mask_bruteforce(seed):
+    """All experts on all tokens, then a one-hot gate mask (einsum-based)
+    equals the oracle's grouped verify_moe + combine."""
+    rng = np.random.default_rng(200 + seed)
+    H, F, E, k, S, Fs = 16, 24, 6, 2, int(seed % 3), 8
+    B = int(rng.integers(1, 9))
+    x = rng.standard_normal((B, H)).astype(np.float32)
+    ex = {"gate": rng.standard_normal((E, F, H)).astype(np.float32) * 0.3,
+          "up": rng.standard_normal((E, F, H)).astype(np.float32) * 0.3,
+          "down": rng.standard_normal((E, H, F)).astype(np.float32) * 0.3}
+    sh = {"gate": rng.standard_normal((S, Fs, H)).astype(np.float32) * 0.3,
+          "up": rng.standard_normal((S, Fs, H)).astype(np.float32) * 0.3,
+          "down": rng.standard_normal((S, H, Fs)).astype(np.float32) * 0.3} if S else {}
+    idx = np.array([np.sort(rng.choice(E, k, replace=False)) for _ in range(B)], np.int32)
+    gw = rng.random((B, k))
+    gw /= gw.sum(1, keepdims=True)
+    eo = oracle.verify_moe(x, ex, sh, {"idx": idx}, k, "f32", "f32", S)
+    y = oracle.combine(gw, eo, k, S)
+
+    X = x.astype(np.float64)
+    a = np.einsum("bh,efh->bef", X, ex["gate"].astype(np.float64))
+    u = np.einsum("bh,efh->bef", X, ex["up"].astype(np.float64))
+    dense = np.einsum("bef,ehf->beh", a * expit(a) * u, ex["down"].astype(np.float64))
+    G = np.zeros((B, E))
+    for b in range(B):
+        G[b, idx[b]] = gw[b]
+    ref = np.einsum("be,beh->bh", G, dense)
+    for s in range(S):
+        a = X @ sh["gate"][s].astype(np.float64).T
+        ref += (a * expit(a) * (X @ sh["up"][s].astype(np.float64).T)) @ sh["down"][s].astype(np.float64).T
+    np.testing.assert_allclose(y, ref, rtol=1e-12, atol=1e-12)
+
+
+def test_int4_dequant_known_codes():
+    """Byte 0x8F holds element 0 = 15 (low nibble) and element 1 = 8 (high);
+    with scale 0.5: w = 0.5 * (15 - 8) = 3.5 and 0.5 * (8 - 8) = 0."""
+    codes = np.zeros((2, 32), np.uint8)          # rows=2, K=64 -> 2 groups per row
+    codes[0, 0] = 0x8F
+    codes[0, 16] = 0x10                          # group 1: elem 32 = 0, elem 33 = 1
+    codes[1, :] = 0x88                           # all exactly zero
+    scales = np.array([[0.5, 0.25], [3.0, 7.0]], np.float16)
+    w = oracle.dequant_q4g32(codes, scales)
+    assert w.shape == (2, 64)
+    assert w[0, 0] == 3.5 and w[0, 1] == 0.0
+    assert w[0, 2] == 0.5 * (0 - 8)
+    assert w[0, 32] == 0.25 * (0 - 8) and w[0, 33] == 0.25 * (1 - 8)
+    assert not w[1].any()
+
+
+# ---------------------------------------------------------------- combine (a10)
+def test_combine_small_numbers():
+    eo = np.array([[1.0, 2.0],     # token 0, slot 0
+                   [10.0, 20.0],   # token 0, slot 1
+                   [3.0, 4.0],     # token 1, slot 0
+                   [30.0, 40.0],   # token 1, slot 1
+                   [100.0, 0.0],   # shared 0, token 0
+                   [0.0, 100.0]])  # shared 0, token 1
+    gw = np.array([[0.25, 0.75], [0.5, 0.5]])
+    y = oracle.combine(gw, eo, 2, 1)
+    np.testing.assert_array_equal(y, [[0.25 + 7.5 + 100.0, 0.5 + 15.0],
+                                      [1.5 + 15.0, 2.0 + 20.0 + 100.0]])
+
+
+# ---------------------------------------------------------------- reuse ratio
+def test_reuse_ratio_bounds_and_identical_tokens():
+    """1/B <= r <= 1 (Sec. Motivation, Challenge 2: the ideal ratio is 1/s);
+    identical tokens activate exactly k experts."""
+    rng = np.random.default_rng(5)
+    E, k = 16, 4
+    for B in (1, 3, 8):
+        idx = np.array([np.sort(rng.choice(E, k, replace=False)) for _ in range(B)])
+        r = oracle.bucket(idx, E)["reuse_ratio"]
+        assert 1.0 / B - 1e-15 <= r <= 1.0
+        same = np.tile(idx[:1], (B, 1))
+        bk = oracle.bucket(same, E)
+        assert bk["n_uniq"] == k and bk["reuse_ratio"] == 1.0 / B
