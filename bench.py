@@ -1,0 +1,165 @@
+"""Verify-MoE layer benchmark on one MI355X.
+
+A step is one full pass of the hot path -- route, reuse-aware gating, grouped
+SwiGLU experts, combine -- over one verify batch of synthetic draft tokens,
+enqueued back to back on one HIP stream with all inputs resident in HBM.
+
+    python bench.py [--steps K] [--warmup W] [--workload c2]
+
+Prints one JSON line.  `value` is draft tokens per second of whole steps;
+`roofline` covers the expert-FFN launches of s2moe_verify_moe (gate-up and
+down), timed with HIP events on the stream they run on, against the unique
+expert weight bytes the step must read; `cpu_baseline` times the fp64 oracle
+on the host for the same step.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
+
+
+def _log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def expert_bytes(shape, F: int) -> int:
+    """HBM bytes of one expert's gate, up and down weights (int4 scales included)."""
+    n = 3 * F * shape.hidden
+    if shape.wdt == "bf16":
+        return 2 * n
+    if shape.wdt == "f32":
+        return 4 * n
+    return n // 2 + 2 * (n // 32)  # 4-bit codes + one fp16 scale per 32
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="c2", choices=["c1", "c2", "c3", "c4", "c5"])
+    ap.add_argument("--batch", type=int, default=None, help="draft tokens (default: workload's)")
+    ap.add_argument("--alpha", type=float, default=None)
+    ap.add_argument("--seed", type=int, default=1)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args(argv)
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the verify-MoE path here runs on a single "
+              "MI355X (no multi-GPU path is built); run it with --gpus 1.", file=sys.stderr)
+        return 2
+
+    import torch
+
+    import paper_2608_15018_amd as s2
+    from synth import gen
+    from synth.configs import WORKLOAD_ID, WORKLOADS
+
+    s2.load()
+    torch.cuda.set_device(0)
+    wl = WORKLOADS[args.workload]
+    shape = wl.shape if args.alpha is None else wl.shape.with_(alpha=args.alpha)
+    B = args.batch or wl.batches[-1 if args.workload == "c5" else 0]
+    wid = WORKLOAD_ID[wl.name]
+
+    t0 = time.time()
+    router = gen.make_router(shape, args.seed, 0, wid, wl.router_std)
+    x, conf_w, _ = gen.make_batch(shape, B, args.seed, 0, wid, wl.rho)
+    experts = gen.make_experts(shape, args.seed, 0, wid, wl.w_std)
+    shared = gen.make_shared_experts(shape, args.seed, 0, wid, wl.w_std)
+    _log(f"[bench] inputs generated in {time.time() - t0:.1f}s")
+
+    layer = s2.make_layer(shape)
+    p = s2.VerifyPass(layer, B)
+    xd, rd, cd = s2.to_device(x), s2.to_device(router), s2.to_device(conf_w)
+    dev_w, wstruct = s2.weights_to_device(experts, shared)
+    stream = torch.cuda.current_stream()
+
+    # warm-up (also fixes the routing, which is deterministic)
+    for _ in range(max(1, args.warmup)):
+        p(xd, rd, cd, wstruct)
+    torch.cuda.synchronize()
+    n_uniq = int(p.rt.n_uniq.item())
+    unique_bytes = n_uniq * expert_bytes(shape, shape.ffn) + \
+        shape.n_shared * expert_bytes(shape, shape.ffn_shared)
+
+    # timed region: K whole steps; events bracket the FFN launches of each step
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for i in range(args.steps):
+        p.route(xd, rd)
+        p.reuse_gate(cd)
+        ev[i][0].record(stream)
+        p.verify_moe(xd, wstruct)
+        ev[i][1].record(stream)
+        p.combine()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t_start
+    ffn_ms = [a.elapsed_time(b) for a, b in ev]
+    ffn_avg_s = float(np.mean(ffn_ms)) / 1e3
+    ms_per_step = elapsed / args.steps * 1e3
+    achieved = unique_bytes / ffn_avg_s / 1e9
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+        try:
+            from threadpoolctl import threadpool_info
+            cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+        except Exception:  # pragma: no cover
+            cores = os.cpu_count()
+        t = time.perf_counter()
+        oracle.forward(x, router, conf_w, experts, shared, shape)
+        dt = time.perf_counter() - t
+        cpu = {"value": B / dt, "unit": "draft tokens/s", "cores": cores, "kind": "oracle",
+               "sample": f"one full verify step of {wl.name} (B={B}, {n_uniq} activated experts"
+                         f"{', %d shared' % shape.n_shared if shape.n_shared else ''}), fp64 "
+                         f"numpy, {dt:.1f}s"}
+
+    out = {
+        "metric": "verify-MoE layer: draft tokens/s and achieved HBM GB/s (% of peak) on "
+                  "unique experts",
+        "value": B * args.steps / elapsed,
+        "unit": "draft tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": {"bf16": "bf16", "f32": "f32", "q4g32": "int4-g32/bf16"}[shape.wdt],
+        "data": "synthetic",
+        "config": {"workload": wl.description, "name": wl.name, "draft_tokens": B,
+                   "hidden": shape.hidden, "ffn": shape.ffn, "experts": shape.n_experts,
+                   "top_k": shape.top_k, "shared": shape.n_shared, "cap": shape.cap,
+                   "alpha": shape.alpha},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "kernel": "s2moe_verify_moe (expert gate-up + down launches)",
+                     "bytes_per_launch": unique_bytes, "avg_launch_us": ffn_avg_s * 1e6},
+        "cpu_baseline": cpu,
+        "n_uniq": n_uniq,
+        "reuse_ratio": n_uniq / (B * shape.top_k),
+        "ffn_us_p10_p90": [float(np.percentile(ffn_ms, 10)) * 1e3,
+                           float(np.percentile(ffn_ms, 90)) * 1e3],
+    }
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,177 @@
+/*
+ * s2moe.h -- C ABI of the S2-MoE verify-MoE hot path on AMD Instinct MI355X
+ * (gfx950).
+ *
+ * The verification pass of self-speculative decoding runs one MoE layer over
+ * the B draft tokens of a verify batch.  The paper (Sec. "Reuse-aware Expert
+ * Gating") defines the routing part: the target gating logits ell_b of each
+ * draft token, confidence weights w_b >= 0, the cross-token expert importance
+ * g_e = sum_b w_b ell_{b,e}, the globally preferred set E* = TopCap(g) with
+ * k <= cap, and the additive bias ell'_{b,e} = ell_{b,e} + lambda_b [e in E*]
+ * with lambda_b proportional to the gap between the token's top-1 and
+ * (k+1)-th logits.  The experts are SwiGLU FFNs; each activated expert's
+ * weights are streamed from HBM once for all tokens routed to it (the
+ * verification cost the paper counts per newly activated expert, Sec.
+ * "Routing-aware Adaptive Speculative Expansion", marginal verification
+ * cost).
+ *
+ * Conventions shared by every entry point
+ *   - Tensor arguments are DEVICE pointers, row-major, owned by the caller.
+ *     The library never allocates or frees device memory.
+ *   - Every pointer must be 16-byte aligned.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *     Calls only enqueue work; results are valid once the stream reaches
+ *     them.  Nothing synchronises the host.
+ *   - Argument errors are detected on the host before anything is enqueued
+ *     and returned as S2MOE_EINVAL / S2MOE_EUNSUPPORTED / S2MOE_EWORKSPACE;
+ *     a failed launch returns S2MOE_EHIP.  s2moe_last_error() then names the
+ *     problem (thread-local string).  No exception crosses the ABI.
+ *   - Non-finite inputs are undefined behaviour.
+ *   - Calls on one stream are ordered; calls that share output buffers on
+ *     different streams race.
+ */
+#ifndef S2MOE_H
+#define S2MOE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define S2MOE_ABI_VERSION 1
+#define S2MOE_MAX_TOKENS 256  /* B: draft tokens per verify batch   */
+#define S2MOE_MAX_EXPERTS 256 /* E: routed experts per layer        */
+#define S2MOE_MAX_TOPK 16     /* k: experts per token               */
+#define S2MOE_MAX_SHARED 8    /* S: always-on shared experts        */
+
+typedef enum s2moe_status {
+  S2MOE_OK = 0,
+  S2MOE_EINVAL = 1,       /* malformed argument (null, misaligned, out of range) */
+  S2MOE_EUNSUPPORTED = 2, /* well-formed but outside what the kernels handle     */
+  S2MOE_EWORKSPACE = 3,   /* workspace missing or smaller than required          */
+  S2MOE_EHIP = 4          /* a HIP launch or runtime call failed                 */
+} s2moe_status;
+
+typedef enum s2moe_dtype {
+  S2MOE_F32 = 0,
+  S2MOE_BF16 = 1,
+  /* weights only: 4-bit codes q in [0,15], two per byte (element 2i in the
+     low nibble of byte i), value s * (q - 8) with one fp16 scale s per 32
+     consecutive elements along K.  Codes [rows, K/2] u8, scales [rows, K/32]
+     f16, per expert. */
+  S2MOE_Q4G32 = 2
+} s2moe_dtype;
+
+/* Readings of the paper's gating where the text leaves a choice (0 = default). */
+enum {
+  /* TopCap candidates restricted to experts in some token's plain top-k
+     ("experts that already exhibit repeated activation"); |E*| <= cap. */
+  S2MOE_PREF_ACTIVATED_ONLY = 1u,
+  /* lambda_b = alpha instead of alpha * gap_b. */
+  S2MOE_BIAS_ABSOLUTE = 2u,
+  /* gate weights from the biased logits ell' instead of the original ell. */
+  S2MOE_GATE_FROM_BIASED = 4u
+};
+
+/* One MoE layer.  Supported (act_dtype, w_dtype) pairs: (F32, F32),
+   (BF16, BF16), (BF16, Q4G32). */
+typedef struct s2moe_layer {
+  int32_t hidden;      /* H: 64 <= H <= 16384, H % 64 == 0                  */
+  int32_t ffn;         /* F: routed SwiGLU width, 64 <= F, F % 64 == 0      */
+  int32_t n_experts;   /* E: 2 <= E <= 256                                  */
+  int32_t top_k;       /* k: 1 <= k < E, k <= 16                            */
+  int32_t n_shared;    /* S: 0 <= S <= 8 always-on experts (weight 1)       */
+  int32_t ffn_shared;  /* F_s: F_s % 64 == 0 when S > 0                     */
+  int32_t cap;         /* k <= cap <= E                                     */
+  float alpha;         /* lambda_b = alpha * gap_b, alpha >= 0, finite      */
+  uint32_t flags;      /* S2MOE_PREF_ACTIVATED_ONLY | ... (default 0)       */
+  int32_t act_dtype;   /* s2moe_dtype of x and router: F32 or BF16          */
+  int32_t w_dtype;     /* s2moe_dtype of expert weights                     */
+} s2moe_layer;
+
+/* Expert weights (device pointers).  Routed:  gate, up [E, F, H] (K = H
+   contiguous), down [E, H, F] (K = F contiguous).  Shared: sh_gate, sh_up
+   [S, F_s, H], sh_down [S, H, F_s].  For Q4G32 the matrices hold codes with
+   K/2 bytes per row and the *_s pointers the fp16 scales with K/32 per row;
+   for F32/BF16 the *_s pointers are ignored. */
+typedef struct s2moe_weights {
+  const void *gate, *up, *down;
+  const void *gate_s, *up_s, *down_s;
+  const void *sh_gate, *sh_up, *sh_down;
+  const void *sh_gate_s, *sh_up_s, *sh_down_s;
+} s2moe_weights;
+
+/* Routing state of one verify batch (device memory, caller-owned).  The
+   pointers are read from this struct; the arrays they name are written. */
+typedef struct s2moe_routing {
+  float *logits;      /* [B, E]   ell_b = W_r x_b (fp32)                       */
+  float *gap;         /* [B]      ell_(1) - ell_(k+1)                          */
+  int32_t *plain_idx; /* [B, k]   unbiased top-k, ascending expert id          */
+  float *g;           /* [E]      sum_b max(w_b, 0) ell_{b,e}                  */
+  int32_t *pref;      /* [E]      1 iff e in E*                                */
+  int32_t *idx;       /* [B, k]   biased top-k, ascending expert id            */
+  float *gate_w;      /* [B, k]   softmax over the selected k, sums to 1       */
+  int32_t *count;     /* [E]      tokens routed to expert e                    */
+  int32_t *offset;    /* [E + 1]  exclusive prefix sum of count                */
+  int32_t *slot;      /* [B * k]  assignments a = b*k + j, expert-major, stable */
+  int32_t *uniq;      /* [E]      activated experts ascending, tail = -1       */
+  int32_t *n_uniq;    /* [1]      |U|                                          */
+} s2moe_routing;
+
+/* Router and plain top-k (Sec. "Reuse-aware Expert Gating": the target
+   gating logits ell_b, and the top-1 / (k+1)-th gap of "Soft routing bias
+   for reuse promotion").
+   x [B, H] and router [E, H] in layer->act_dtype.  Writes r->logits
+   (fp32 accumulation), r->plain_idx (ties -> lower expert id) and r->gap. */
+s2moe_status s2moe_route(const s2moe_layer *layer, int32_t n_tokens, const void *x,
+                         const void *router, const s2moe_routing *r, void *stream);
+
+/* Reuse-aware expert gating and token->expert bucketing (same section:
+   "Cross-token expert importance aggregation", "Global preferred expert
+   selection", "Soft routing bias for reuse promotion").
+   conf_w [B] fp32; values below 0 are treated as 0 and if none is positive
+   no bias is applied.  Reads r->logits, r->gap, r->plain_idx; writes r->g,
+   pref, idx, gate_w, count, offset, slot, uniq, n_uniq.  Deterministic: no
+   floating-point atomics, fixed summation order. */
+s2moe_status s2moe_reuse_gate(const s2moe_layer *layer, int32_t n_tokens,
+                              const float *conf_w, const s2moe_routing *r, void *stream);
+
+/* Bytes of device workspace s2moe_verify_moe needs for n_tokens tokens. */
+size_t s2moe_workspace_bytes(const s2moe_layer *layer, int32_t n_tokens);
+
+/* Grouped SwiGLU experts over the verify batch: for every activated expert
+   e, FFN_e(x) = W_d,e (silu(W_g,e x) * (W_u,e x)) of each token routed to it,
+   each expert's weights read from HBM once for all its tokens; and every
+   shared expert over all tokens.
+   x [B, H] act_dtype; reads r->count, offset, slot, uniq, n_uniq.  Writes
+   expert_out [B*k + S*B, H] fp32, unscaled: row b*k + j for the j-th routed
+   expert of token b, row B*k + s*B + b for shared expert s.  workspace must
+   hold s2moe_workspace_bytes(layer, n_tokens) bytes; its contents on entry
+   do not matter and are clobbered. */
+s2moe_status s2moe_verify_moe(const s2moe_layer *layer, int32_t n_tokens, const void *x,
+                              const s2moe_weights *w, const s2moe_routing *r,
+                              void *workspace, size_t workspace_bytes, float *expert_out,
+                              void *stream);
+
+/* Combine: y_b = sum_{j<k} gate_w[b,j] expert_out[b*k+j] +
+   sum_{s<S} expert_out[B*k + s*B + b], summed in that order (fp32). */
+s2moe_status s2moe_combine(const s2moe_layer *layer, int32_t n_tokens,
+                           const s2moe_routing *r, const float *expert_out, float *y,
+                           void *stream);
+
+/* Message of the last failed call on this thread ("" if none). */
+const char *s2moe_last_error(void);
+
+/* Static name of a status code. */
+const char *s2moe_status_string(s2moe_status status);
+
+/* S2MOE_ABI_VERSION of the loaded library. */
+int32_t s2moe_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* S2MOE_H */

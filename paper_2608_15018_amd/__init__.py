@@ -1,0 +1,28 @@
+"""S2-MoE verify-MoE hot path for AMD Instinct MI355X (gfx950).
+
+The work happens in libs2moe.so (hand-written HIP, C ABI in include/s2moe.h);
+this package is its thin Python binding.
+"""
+
+from ._lib import (  # noqa: F401
+    BF16,
+    BIAS_ABSOLUTE,
+    F32,
+    GATE_FROM_BIASED,
+    PREF_ACTIVATED_ONLY,
+    Q4G32,
+    Layer,
+    Routing,
+    S2moeError,
+    Weights,
+    abi_version,
+    combine,
+    load,
+    make_layer,
+    make_weights,
+    reuse_gate,
+    route,
+    verify_moe,
+    workspace_bytes,
+)
+from .pipeline import VerifyPass, to_device, weights_to_device  # noqa: F401

@@ -1,0 +1,296 @@
+// C-ABI entry points: argument validation on the host, then kernel launches
+// on the caller's stream.  Nothing here allocates device memory.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdint>
+#include <cstdio>
+#include <string>
+
+#include "kernels.h"
+#include "s2moe.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+s2moe_status fail(s2moe_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return st;
+}
+
+s2moe_status ok() {
+  g_last_error.clear();
+  return S2MOE_OK;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+#define S2MOE_REQUIRE_PTR(p)                                                     \
+  do {                                                                           \
+    if ((p) == nullptr) return fail(S2MOE_EINVAL, "%s: %s is NULL", fn, #p);     \
+    if (!aligned16(p)) return fail(S2MOE_EINVAL, "%s: %s is not 16-byte aligned", fn, #p); \
+  } while (0)
+
+s2moe_status check_layer(const char* fn, const s2moe_layer* L, int32_t B) {
+  if (L == nullptr) return fail(S2MOE_EINVAL, "%s: layer is NULL", fn);
+  if (B < 1) return fail(S2MOE_EINVAL, "%s: n_tokens = %d, must be >= 1", fn, B);
+  if (B > S2MOE_MAX_TOKENS)
+    return fail(S2MOE_EUNSUPPORTED, "%s: n_tokens = %d exceeds %d", fn, B, S2MOE_MAX_TOKENS);
+  if (L->hidden < 64 || L->hidden % 64 != 0 || L->hidden > 65536)
+    return fail(S2MOE_EINVAL, "%s: hidden = %d must be a multiple of 64 in [64, 65536]", fn,
+                L->hidden);
+  if (L->ffn < 64 || L->ffn % 64 != 0 || L->ffn > 262144)
+    return fail(S2MOE_EINVAL, "%s: ffn = %d must be a multiple of 64 in [64, 262144]", fn,
+                L->ffn);
+  if (L->n_experts < 2)
+    return fail(S2MOE_EINVAL, "%s: n_experts = %d must be >= 2", fn, L->n_experts);
+  if (L->n_experts > S2MOE_MAX_EXPERTS)
+    return fail(S2MOE_EUNSUPPORTED, "%s: n_experts = %d exceeds %d", fn, L->n_experts,
+                S2MOE_MAX_EXPERTS);
+  if (L->top_k < 1 || L->top_k >= L->n_experts)
+    return fail(S2MOE_EINVAL, "%s: top_k = %d must satisfy 1 <= k < E = %d", fn, L->top_k,
+                L->n_experts);
+  if (L->top_k > S2MOE_MAX_TOPK)
+    return fail(S2MOE_EUNSUPPORTED, "%s: top_k = %d exceeds %d", fn, L->top_k, S2MOE_MAX_TOPK);
+  if (L->cap < L->top_k || L->cap > L->n_experts)
+    return fail(S2MOE_EINVAL, "%s: cap = %d must satisfy k = %d <= cap <= E = %d", fn, L->cap,
+                L->top_k, L->n_experts);
+  if (!std::isfinite(L->alpha) || L->alpha < 0.f)
+    return fail(S2MOE_EINVAL, "%s: alpha = %g must be finite and >= 0", fn, (double)L->alpha);
+  if (L->flags & ~7u) return fail(S2MOE_EINVAL, "%s: unknown flags 0x%x", fn, L->flags);
+  if (L->n_shared < 0) return fail(S2MOE_EINVAL, "%s: n_shared = %d < 0", fn, L->n_shared);
+  if (L->n_shared > S2MOE_MAX_SHARED)
+    return fail(S2MOE_EUNSUPPORTED, "%s: n_shared = %d exceeds %d", fn, L->n_shared,
+                S2MOE_MAX_SHARED);
+  if (L->n_shared > 0 && (L->ffn_shared < 64 || L->ffn_shared % 64 != 0 ||
+                          L->ffn_shared > 262144))
+    return fail(S2MOE_EINVAL, "%s: ffn_shared = %d must be a multiple of 64 in [64, 262144]",
+                fn, L->ffn_shared);
+  const int act = L->act_dtype, wdt = L->w_dtype;
+  if (act != S2MOE_F32 && act != S2MOE_BF16)
+    return fail(S2MOE_EINVAL, "%s: act_dtype = %d must be F32 or BF16", fn, act);
+  if (wdt != S2MOE_F32 && wdt != S2MOE_BF16 && wdt != S2MOE_Q4G32)
+    return fail(S2MOE_EINVAL, "%s: w_dtype = %d is not a known dtype", fn, wdt);
+  const bool pair_ok = (act == S2MOE_F32 && wdt == S2MOE_F32) ||
+                       (act == S2MOE_BF16 && (wdt == S2MOE_BF16 || wdt == S2MOE_Q4G32));
+  if (!pair_ok)
+    return fail(S2MOE_EUNSUPPORTED,
+                "%s: (act_dtype, w_dtype) = (%d, %d); supported: (F32, F32), (BF16, BF16), "
+                "(BF16, Q4G32)",
+                fn, act, wdt);
+  if (wdt == S2MOE_Q4G32 &&
+      (L->hidden % 256 || L->ffn % 256 || (L->n_shared > 0 && L->ffn_shared % 256)))
+    return fail(S2MOE_EUNSUPPORTED,
+                "%s: Q4G32 weights need hidden, ffn and ffn_shared multiples of 256", fn);
+  return S2MOE_OK;
+}
+
+size_t workspace_bytes(const s2moe_layer* L, int32_t B) {
+  const size_t rows = (size_t)B * L->top_k + (size_t)L->n_shared * B;
+  const size_t ldh = (size_t)(L->n_shared > 0 && L->ffn_shared > L->ffn ? L->ffn_shared : L->ffn);
+  const size_t elt = L->w_dtype == S2MOE_F32 ? 4 : 2;
+  return (rows * ldh * elt + 255) & ~(size_t)255;
+}
+
+s2moe_status hip_status(const char* fn, hipError_t err) {
+  if (err != hipSuccess) return fail(S2MOE_EHIP, "%s: %s", fn, hipGetErrorString(err));
+  return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t s2moe_abi_version(void) { return S2MOE_ABI_VERSION; }
+
+const char* s2moe_last_error(void) { return g_last_error.c_str(); }
+
+const char* s2moe_status_string(s2moe_status st) {
+  switch (st) {
+    case S2MOE_OK: return "S2MOE_OK";
+    case S2MOE_EINVAL: return "S2MOE_EINVAL";
+    case S2MOE_EUNSUPPORTED: return "S2MOE_EUNSUPPORTED";
+    case S2MOE_EWORKSPACE: return "S2MOE_EWORKSPACE";
+    case S2MOE_EHIP: return "S2MOE_EHIP";
+  }
+  return "S2MOE_UNKNOWN";
+}
+
+s2moe_status s2moe_route(const s2moe_layer* layer, int32_t n_tokens, const void* x,
+                         const void* router, const s2moe_routing* r, void* stream) {
+  const char* fn = "s2moe_route";
+  s2moe_status st = check_layer(fn, layer, n_tokens);
+  if (st != S2MOE_OK) return st;
+  if (r == nullptr) return fail(S2MOE_EINVAL, "%s: routing is NULL", fn);
+  S2MOE_REQUIRE_PTR(x);
+  S2MOE_REQUIRE_PTR(router);
+  S2MOE_REQUIRE_PTR(r->logits);
+  S2MOE_REQUIRE_PTR(r->gap);
+  S2MOE_REQUIRE_PTR(r->plain_idx);
+  s2moe::RouteArgs a;
+  a.x = x;
+  a.router = router;
+  a.logits = r->logits;
+  a.plain_idx = r->plain_idx;
+  a.gap = r->gap;
+  a.B = n_tokens;
+  a.H = layer->hidden;
+  a.E = layer->n_experts;
+  a.k = layer->top_k;
+  a.bf16 = layer->act_dtype == S2MOE_BF16;
+  return hip_status(fn, s2moe::launch_route(a, static_cast<hipStream_t>(stream)));
+}
+
+s2moe_status s2moe_reuse_gate(const s2moe_layer* layer, int32_t n_tokens, const float* conf_w,
+                              const s2moe_routing* r, void* stream) {
+  const char* fn = "s2moe_reuse_gate";
+  s2moe_status st = check_layer(fn, layer, n_tokens);
+  if (st != S2MOE_OK) return st;
+  if (r == nullptr) return fail(S2MOE_EINVAL, "%s: routing is NULL", fn);
+  S2MOE_REQUIRE_PTR(conf_w);
+  S2MOE_REQUIRE_PTR(r->logits);
+  S2MOE_REQUIRE_PTR(r->gap);
+  S2MOE_REQUIRE_PTR(r->plain_idx);
+  S2MOE_REQUIRE_PTR(r->g);
+  S2MOE_REQUIRE_PTR(r->pref);
+  S2MOE_REQUIRE_PTR(r->idx);
+  S2MOE_REQUIRE_PTR(r->gate_w);
+  S2MOE_REQUIRE_PTR(r->count);
+  S2MOE_REQUIRE_PTR(r->offset);
+  S2MOE_REQUIRE_PTR(r->slot);
+  S2MOE_REQUIRE_PTR(r->uniq);
+  S2MOE_REQUIRE_PTR(r->n_uniq);
+  s2moe::GateArgs a;
+  a.logits = r->logits;
+  a.gap = r->gap;
+  a.plain_idx = r->plain_idx;
+  a.conf_w = conf_w;
+  a.g = r->g;
+  a.pref = r->pref;
+  a.idx = r->idx;
+  a.gate_w = r->gate_w;
+  a.count = r->count;
+  a.offset = r->offset;
+  a.slot = r->slot;
+  a.uniq = r->uniq;
+  a.n_uniq = r->n_uniq;
+  a.B = n_tokens;
+  a.E = layer->n_experts;
+  a.k = layer->top_k;
+  a.cap = layer->cap;
+  a.alpha = layer->alpha;
+  a.flags = layer->flags;
+  return hip_status(fn, s2moe::launch_reuse_gate(a, static_cast<hipStream_t>(stream)));
+}
+
+size_t s2moe_workspace_bytes(const s2moe_layer* layer, int32_t n_tokens) {
+  if (check_layer("s2moe_workspace_bytes", layer, n_tokens) != S2MOE_OK) return 0;
+  return workspace_bytes(layer, n_tokens);
+}
+
+s2moe_status s2moe_verify_moe(const s2moe_layer* layer, int32_t n_tokens, const void* x,
+                              const s2moe_weights* w, const s2moe_routing* r, void* workspace,
+                              size_t workspace_bytes_given, float* expert_out, void* stream) {
+  const char* fn = "s2moe_verify_moe";
+  s2moe_status st = check_layer(fn, layer, n_tokens);
+  if (st != S2MOE_OK) return st;
+  if (w == nullptr) return fail(S2MOE_EINVAL, "%s: weights is NULL", fn);
+  if (r == nullptr) return fail(S2MOE_EINVAL, "%s: routing is NULL", fn);
+  S2MOE_REQUIRE_PTR(x);
+  S2MOE_REQUIRE_PTR(expert_out);
+  S2MOE_REQUIRE_PTR(w->gate);
+  S2MOE_REQUIRE_PTR(w->up);
+  S2MOE_REQUIRE_PTR(w->down);
+  const bool q4 = layer->w_dtype == S2MOE_Q4G32;
+  if (q4) {
+    S2MOE_REQUIRE_PTR(w->gate_s);
+    S2MOE_REQUIRE_PTR(w->up_s);
+    S2MOE_REQUIRE_PTR(w->down_s);
+  }
+  if (layer->n_shared > 0) {
+    S2MOE_REQUIRE_PTR(w->sh_gate);
+    S2MOE_REQUIRE_PTR(w->sh_up);
+    S2MOE_REQUIRE_PTR(w->sh_down);
+    if (q4) {
+      S2MOE_REQUIRE_PTR(w->sh_gate_s);
+      S2MOE_REQUIRE_PTR(w->sh_up_s);
+      S2MOE_REQUIRE_PTR(w->sh_down_s);
+    }
+  }
+  S2MOE_REQUIRE_PTR(r->count);
+  S2MOE_REQUIRE_PTR(r->offset);
+  S2MOE_REQUIRE_PTR(r->slot);
+  S2MOE_REQUIRE_PTR(r->uniq);
+  S2MOE_REQUIRE_PTR(r->n_uniq);
+  const size_t need = workspace_bytes(layer, n_tokens);
+  if (workspace == nullptr)
+    return fail(S2MOE_EWORKSPACE, "%s: workspace is NULL (%zu bytes needed)", fn, need);
+  if (!aligned16(workspace))
+    return fail(S2MOE_EINVAL, "%s: workspace is not 16-byte aligned", fn);
+  if (workspace_bytes_given < need)
+    return fail(S2MOE_EWORKSPACE, "%s: workspace holds %zu bytes, %zu needed", fn,
+                workspace_bytes_given, need);
+
+  s2moe::FfnArgs a;
+  a.B = n_tokens;
+  a.k = layer->top_k;
+  a.S = layer->n_shared;
+  a.E = layer->n_experts;
+  a.H = layer->hidden;
+  a.F = layer->ffn;
+  a.Fs = layer->n_shared > 0 ? layer->ffn_shared : 0;
+  a.wf = layer->w_dtype == S2MOE_F32 ? s2moe::kWF32
+                                     : (q4 ? s2moe::kWQ4 : s2moe::kWBf16);
+  a.count = r->count;
+  a.offset = r->offset;
+  a.slot = r->slot;
+  a.uniq = r->uniq;
+  a.n_uniq = r->n_uniq;
+  a.x = x;
+  a.gate = w->gate;
+  a.up = w->up;
+  a.down = w->down;
+  a.gate_s = w->gate_s;
+  a.up_s = w->up_s;
+  a.down_s = w->down_s;
+  a.sh_gate = w->sh_gate;
+  a.sh_up = w->sh_up;
+  a.sh_down = w->sh_down;
+  a.sh_gate_s = w->sh_gate_s;
+  a.sh_up_s = w->sh_up_s;
+  a.sh_down_s = w->sh_down_s;
+  a.hh = workspace;
+  a.ldh = (layer->n_shared > 0 && layer->ffn_shared > layer->ffn) ? layer->ffn_shared
+                                                                   : layer->ffn;
+  a.out = expert_out;
+  return hip_status(fn, s2moe::launch_ffn(a, static_cast<hipStream_t>(stream)));
+}
+
+s2moe_status s2moe_combine(const s2moe_layer* layer, int32_t n_tokens, const s2moe_routing* r,
+                           const float* expert_out, float* y, void* stream) {
+  const char* fn = "s2moe_combine";
+  s2moe_status st = check_layer(fn, layer, n_tokens);
+  if (st != S2MOE_OK) return st;
+  if (r == nullptr) return fail(S2MOE_EINVAL, "%s: routing is NULL", fn);
+  S2MOE_REQUIRE_PTR(r->gate_w);
+  S2MOE_REQUIRE_PTR(expert_out);
+  S2MOE_REQUIRE_PTR(y);
+  s2moe::CombineArgs a;
+  a.gate_w = r->gate_w;
+  a.expert_out = expert_out;
+  a.y = y;
+  a.B = n_tokens;
+  a.H = layer->hidden;
+  a.k = layer->top_k;
+  a.S = layer->n_shared;
+  return hip_status(fn, s2moe::launch_combine(a, static_cast<hipStream_t>(stream)));
+}
+
+}  // extern "C"

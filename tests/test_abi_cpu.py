@@ -1,0 +1,123 @@
+"""C-ABI checks that need no GPU: the library loads, exports every function
+the header declares, and rejects malformed arguments on the host before
+anything is enqueued (no kernel is launched by these tests)."""
+
+import ctypes
+import subprocess
+
+import pytest
+
+import paper_2608_15018_amd as s2
+from paper_2608_15018_amd import _lib
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return s2.load()
+
+
+def test_exports_every_declared_function(lib):
+    declared = _lib.header_functions()
+    assert {"s2moe_route", "s2moe_reuse_gate", "s2moe_verify_moe", "s2moe_combine",
+            "s2moe_workspace_bytes", "s2moe_last_error"} <= set(declared)
+    out = subprocess.run(["nm", "-D", "--defined-only", _lib.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = {line.split()[-1] for line in out.splitlines() if line.strip()}
+    for name in declared:
+        assert name in exported, name
+        assert hasattr(lib, name)
+
+
+def test_version_and_status_strings(lib):
+    assert s2.abi_version() == 1
+    assert lib.s2moe_status_string(0) == b"S2MOE_OK"
+    assert lib.s2moe_status_string(3) == b"S2MOE_EWORKSPACE"
+
+
+def _layer(**kw):
+    base = dict(hidden=256, ffn=512, n_experts=8, top_k=2, cap=4, alpha=0.5, act="bf16",
+                wdt="bf16")
+    base.update(kw)
+    return s2.make_layer(**base)
+
+
+def _route_status(lib, layer, B=4, ptrs=True):
+    # Aligned fake addresses; every case below fails validation before use.
+    fake = ctypes.c_void_p(0x100000) if ptrs else None
+    rt = _lib.RoutingStruct(*([0x200000] * 12))
+    st = lib.s2moe_route(ctypes.byref(layer) if layer is not None else None, B, fake, fake,
+                         ctypes.byref(rt), None)
+    return st, _lib.last_error()
+
+
+@pytest.mark.parametrize("kw,B,status,needle", [
+    ({}, 0, _lib.EINVAL, "n_tokens"),
+    ({}, 257, _lib.EUNSUPPORTED, "n_tokens"),
+    ({"hidden": 100}, 4, _lib.EINVAL, "hidden"),
+    ({"ffn": 96}, 4, _lib.EINVAL, "ffn"),
+    ({"n_experts": 300, "cap": 4}, 4, _lib.EUNSUPPORTED, "n_experts"),
+    ({"top_k": 8}, 4, _lib.EINVAL, "top_k"),
+    ({"n_experts": 64, "top_k": 17, "cap": 20}, 4, _lib.EUNSUPPORTED, "top_k"),
+    ({"cap": 1}, 4, _lib.EINVAL, "cap"),
+    ({"cap": 9}, 4, _lib.EINVAL, "cap"),
+    ({"alpha": -1.0}, 4, _lib.EINVAL, "alpha"),
+    ({"alpha": float("inf")}, 4, _lib.EINVAL, "alpha"),
+    ({"flags": 8}, 4, _lib.EINVAL, "flags"),
+    ({"n_shared": 2, "ffn_shared": 0}, 4, _lib.EINVAL, "ffn_shared"),
+    ({"n_shared": 9, "ffn_shared": 64}, 4, _lib.EUNSUPPORTED, "n_shared"),
+    ({"act": "f32", "wdt": "bf16"}, 4, _lib.EUNSUPPORTED, "supported"),
+    ({"act": "q4g32"}, 4, _lib.EINVAL, "act_dtype"),
+    ({"wdt": "q4g32", "ffn": 320}, 4, _lib.EUNSUPPORTED, "Q4G32"),
+])
+def test_invalid_layers_rejected_on_host(lib, kw, B, status, needle):
+    st, msg = _route_status(lib, _layer(**kw), B)
+    assert st == status, msg
+    assert needle in msg
+
+
+def test_null_and_misaligned_pointers(lib):
+    L = _layer()
+    st, msg = _route_status(lib, None)
+    assert st == _lib.EINVAL and "layer" in msg
+    st, msg = _route_status(lib, L, ptrs=False)
+    assert st == _lib.EINVAL and "NULL" in msg
+    rt = _lib.RoutingStruct(*([0x200000] * 12))
+    st = lib.s2moe_route(ctypes.byref(L), 4, ctypes.c_void_p(0x100004), ctypes.c_void_p(0x100000),
+                         ctypes.byref(rt), None)
+    assert st == _lib.EINVAL and "aligned" in _lib.last_error()
+    st = lib.s2moe_reuse_gate(ctypes.byref(L), 4, ctypes.c_void_p(0x100000), None, None)
+    assert st == _lib.EINVAL and "routing" in _lib.last_error()
+
+
+def test_workspace_size_and_errors(lib):
+    L = _layer(n_shared=1, ffn_shared=1024)
+    B = 8
+    need = s2.workspace_bytes(L, B)
+    rows = B * 2 + 1 * B
+    assert need >= rows * 1024 * 2 and need % 256 == 0
+    assert s2.workspace_bytes(_layer(act="f32", wdt="f32"), 8) >= 16 * 512 * 4
+    w = _lib.Weights(*([0x300000] * 12))
+    rt = _lib.RoutingStruct(*([0x200000] * 12))
+    fake = ctypes.c_void_p(0x100000)
+    st = lib.s2moe_verify_moe(ctypes.byref(L), B, fake, ctypes.byref(w), ctypes.byref(rt),
+                              None, need, fake, None)
+    assert st == _lib.EWORKSPACE and "workspace" in _lib.last_error()
+    st = lib.s2moe_verify_moe(ctypes.byref(L), B, fake, ctypes.byref(w), ctypes.byref(rt),
+                              ctypes.c_void_p(0x400000), need - 1, fake, None)
+    assert st == _lib.EWORKSPACE and str(need) in _lib.last_error()
+    w.sh_down = None
+    st = lib.s2moe_verify_moe(ctypes.byref(L), B, fake, ctypes.byref(w), ctypes.byref(rt),
+                              ctypes.c_void_p(0x400000), need, fake, None)
+    assert st == _lib.EINVAL and "sh_down" in _lib.last_error()
+    Lq = _layer(wdt="q4g32")
+    w = _lib.Weights(*([0x300000] * 3 + [None] * 9))
+    st = lib.s2moe_verify_moe(ctypes.byref(Lq), B, fake, ctypes.byref(w), ctypes.byref(rt),
+                              ctypes.c_void_p(0x400000), 1 << 30, fake, None)
+    assert st == _lib.EINVAL and "gate_s" in _lib.last_error()
+    assert lib.s2moe_workspace_bytes(ctypes.byref(_layer(cap=0)), 4) == 0
+
+
+def test_binding_raises_with_message():
+    with pytest.raises(s2.S2moeError) as ei:
+        s2.workspace_bytes(_layer(top_k=0), 4)
+    assert ei.value.status == _lib.EINVAL

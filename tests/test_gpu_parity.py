@@ -1,0 +1,249 @@
+"""GPU parity: the HIP path through the C ABI against the fp64 oracle.
+
+Routing decisions (plain_idx, pref, idx, count, offset, slot, uniq,
+n_uniq) must match bit for bit; the inputs are drawn so that every ranking
+decision is separated by >= 1e-3 (in fp64, on the stored values), which makes
+the decision the same in fp32 and fp64.  Floating-point outputs must be
+within the stated tolerances (max-abs error over max-abs reference).
+"""
+
+import numpy as np
+import pytest
+
+import oracle
+from synth.configs import WORKLOAD_ID, WORKLOADS, LayerShape
+from tests.gpu_helpers import (check_outputs, check_routing, log, make_inputs, rel_err,
+                               run_gpu)
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2608_15018_amd as s2
+    s2.load()
+
+
+def _oracle(shape, d):
+    return oracle.forward(d["x"], d["router"], d["conf_w"], d["experts"], d["shared"], shape)
+
+
+def _full_check(shape, d, label):
+    log(f"[parity] {label}: B={d['x'].shape[0]} H={shape.hidden} F={shape.ffn} "
+        f"E={shape.n_experts} k={shape.top_k} S={shape.n_shared} wdt={shape.wdt}")
+    got, _ = run_gpu(shape, d)
+    ref = _oracle(shape, d)
+    check_routing(got, ref, label)
+    errs = check_outputs(got, ref, shape.wdt, label)
+    log(f"[parity] {label}: ok n_uniq={got['n_uniq']} errs={errs}")
+    return got, ref
+
+
+# Reduced shapes that keep each workload's routing structure and still span
+# several 64-row blocks, several K blocks and ragged token tiles.
+SMALL = {
+    "c1": (WORKLOADS["c1"].shape, 8, 0.0, 0.02),
+    "c2s": (LayerShape(hidden=512, ffn=1024, n_experts=8, top_k=2, cap=4, alpha=0.5), 16, 0.6,
+            None),
+    "c3s": (LayerShape(hidden=256, ffn=256, n_experts=128, top_k=8, cap=14, alpha=0.5), 32,
+            0.5, None),
+    "c4s": (LayerShape(hidden=256, ffn=192, n_experts=64, top_k=6, n_shared=2, ffn_shared=128,
+                       cap=16, alpha=0.5), 64, 0.4, None),
+    "c5s": (LayerShape(hidden=512, ffn=768, n_experts=8, top_k=2, cap=4, alpha=0.5,
+                       wdt="q4g32"), 16, 0.6, None),
+}
+
+
+@pytest.mark.parametrize("name", list(SMALL))
+def test_small_workloads(name):
+    shape, B, rho, rstd = SMALL[name]
+    d = make_inputs(shape, B, seed=101, rho=rho, router_std=rstd)
+    _full_check(shape, d, name)
+
+
+@pytest.mark.parametrize("alpha", [0.0, 0.5, 1.0])
+def test_alpha_sweep_small(alpha):
+    shape = SMALL["c3s"][0].with_(alpha=alpha)
+    d = make_inputs(shape, 32, seed=7, rho=0.5, alphas=(alpha,))
+    got, ref = _full_check(shape, d, f"c3s alpha={alpha}")
+    if alpha == 0.0:
+        np.testing.assert_array_equal(got["idx"], got["plain_idx"])
+
+
+@pytest.mark.parametrize("B", [1, 4, 16, 64])
+def test_int4_draft_sizes_small(B):
+    shape = SMALL["c5s"][0]
+    d = make_inputs(shape, B, seed=300 + B, rho=0.6)
+    _full_check(shape, d, f"c5s B={B}")
+
+
+@pytest.mark.parametrize("flags", [1, 2, 4, 7])
+def test_gating_variants(flags):
+    shape = SMALL["c3s"][0].with_(flags=flags, alpha=0.8)
+    d = make_inputs(shape, 32, seed=50 + flags, rho=0.5, alphas=(0.8,))
+    _full_check(shape, d, f"flags={flags}")
+
+
+def test_single_token():
+    shape = SMALL["c2s"][0]
+    d = make_inputs(shape, 1, seed=3, rho=0.6)
+    got, _ = _full_check(shape, d, "B=1")
+    np.testing.assert_array_equal(got["idx"], got["plain_idx"])
+
+
+def test_max_tokens_one_hot_expert_load():
+    """B = 256 (the ABI maximum) with strongly shared routing, so single
+    experts receive far more than 64 tokens (several token passes)."""
+    shape = LayerShape(hidden=256, ffn=256, n_experts=8, top_k=2, cap=4, alpha=0.5)
+    d = make_inputs(shape, 256, seed=9, rho=0.95)
+    got, _ = _full_check(shape, d, "B=256")
+    assert got["count"].max() > 64
+
+
+def test_max_experts_and_topk():
+    shape = LayerShape(hidden=128, ffn=128, n_experts=256, top_k=16, cap=40, alpha=0.5)
+    d = make_inputs(shape, 24, seed=4, rho=0.5)
+    _full_check(shape, d, "E=256 k=16")
+
+
+def test_cap_equal_E_and_identical_tokens():
+    shape = LayerShape(hidden=256, ffn=256, n_experts=16, top_k=3, cap=16, alpha=0.9)
+    d = make_inputs(shape, 12, seed=5, rho=0.5)
+    got, _ = _full_check(shape, d, "cap=E")
+    np.testing.assert_array_equal(got["idx"], got["plain_idx"])
+    shape2 = shape.with_(cap=6)
+    d2 = dict(d, x=np.tile(d["x"][:1], (12, 1)))
+    got2, _ = _full_check(shape2, d2, "identical tokens")
+    assert got2["n_uniq"] == 3
+
+
+@pytest.mark.parametrize("kind", ["zero", "negative", "mixed"])
+def test_degenerate_confidences(kind):
+    shape = SMALL["c3s"][0]
+    d = make_inputs(shape, 32, seed=21, rho=0.5)
+    w = d["conf_w"].copy()
+    if kind == "zero":
+        w[:] = 0
+    elif kind == "negative":
+        w = -w
+    else:
+        w[::2] = -w[::2]
+    d["conf_w"] = w.astype(np.float32)
+    if kind == "mixed":
+        # redraw so the margins hold for the changed confidences
+        r = oracle.margin_reject(shape.top_k, shape.cap, (shape.alpha,), shape.act)
+        from synth import gen
+        d["x"], _, _ = gen.make_batch(shape, 32, 21, 0, 0, 0.5,
+                                      lambda x, _w: r(x, d["conf_w"], d["router"]))
+    got, _ = _full_check(shape, d, f"conf {kind}")
+    if kind != "mixed":
+        assert got["pref"].sum() == 0
+        np.testing.assert_array_equal(got["idx"], got["plain_idx"])
+
+
+def test_deterministic_bitwise():
+    shape = SMALL["c4s"][0]
+    d = make_inputs(shape, 64, seed=77, rho=0.4)
+    a, dw = run_gpu(shape, d)
+    b, _ = run_gpu(shape, d, dw)
+    for n in ("logits", "gap", "g", "gate_w", "expert_out", "y"):
+        assert np.array_equal(a[n], b[n]), n
+    for n in ("idx", "slot", "uniq"):
+        np.testing.assert_array_equal(a[n], b[n])
+
+
+def test_exact_ties_resolved_by_lower_index():
+    """Dyadic logits (exact in fp32 and fp64) with many exact ties, written
+    straight into the logits buffer; only reuse_gate runs."""
+    import paper_2608_15018_amd as s2
+    rng = np.random.default_rng(0)
+    B, E, k, cap = 32, 24, 4, 8
+    ell = rng.integers(-8, 8, size=(B, E)).astype(np.float64) / 4.0   # many ties
+    w = rng.integers(0, 5, size=B).astype(np.float32) / 4.0
+    plain = np.array([oracle.s2moe_oracle.top_k_ascending(r, k) for r in ell], np.int32)
+    gap = np.array([np.sort(r)[::-1][0] - np.sort(r)[::-1][k] for r in ell])
+    for alpha, flags in ((0.5, 0), (1.0, 0), (0.25, 2), (0.5, 1)):
+        ref = oracle.reuse_gate(ell, gap, plain, w, k, cap, alpha, flags)
+        L = s2.make_layer(hidden=64, ffn=64, n_experts=E, top_k=k, cap=cap, alpha=alpha,
+                          flags=flags)
+        rt = s2.Routing(L, B)
+        rt.logits.copy_(torch.from_numpy(ell.astype(np.float32)))
+        rt.gap.copy_(torch.from_numpy(gap.astype(np.float32)))
+        rt.plain_idx.copy_(torch.from_numpy(plain))
+        s2.reuse_gate(L, torch.from_numpy(w).cuda(), rt)
+        torch.cuda.synchronize()
+        got = rt.host()
+        for n in ("pref", "idx", "count", "offset", "slot", "uniq"):
+            np.testing.assert_array_equal(got[n], ref[n], err_msg=f"{n} alpha={alpha} f={flags}")
+        np.testing.assert_array_equal(got["g"], ref["g"].astype(np.float32))
+        assert np.abs(got["gate_w"] - ref["gate_w"]).max() <= 1e-6
+
+
+# ---------------------------------------------------------------- full sizes
+def _workload_inputs(name, B, seed, layer=0, alphas=None):
+    wl = WORKLOADS[name]
+    return make_inputs(wl.shape, B, seed, rho=wl.rho, router_std=wl.router_std,
+                       alphas=alphas or (wl.shape.alpha,), layer=layer,
+                       wl_id=WORKLOAD_ID[name], w_std=wl.w_std)
+
+
+def test_full_c2_mixtral_bf16():
+    wl = WORKLOADS["c2"]
+    d = _workload_inputs("c2", 16, seed=1)
+    got, ref = _full_check(wl.shape, d, "c2 full")
+    log(f"[parity] c2 reuse ratio {ref['reuse_ratio']:.3f}")
+
+
+def test_full_c3_alpha_sweep():
+    wl = WORKLOADS["c3"]
+    d = _workload_inputs("c3", 32, seed=1, alphas=wl.alphas)
+    from paper_2608_15018_amd.pipeline import weights_to_device
+    dw = weights_to_device(d["experts"], d["shared"])
+    ratios = {}
+    for alpha in wl.alphas:
+        shape = wl.shape.with_(alpha=alpha)
+        log(f"[parity] c3 full alpha={alpha}")
+        got, _ = run_gpu(shape, d, dw)
+        ref = _oracle(shape, d)
+        check_routing(got, ref, f"c3 alpha={alpha}")
+        check_outputs(got, ref, "bf16", f"c3 alpha={alpha}")
+        ratios[alpha] = ref["reuse_ratio"]
+    log(f"[parity] c3 reuse ratio by alpha: {ratios}")
+    assert ratios[1.0] <= ratios[0.0]
+
+
+def test_full_c4_shared_routed():
+    wl = WORKLOADS["c4"]
+    d = _workload_inputs("c4", 64, seed=1)
+    _full_check(wl.shape, d, "c4 full")
+
+
+def test_full_c5_int4_layers():
+    """Mixtral-shaped int4 layers at draft sizes 1, 4, 16, 64 (layer 0) and
+    16 (layer 23).  The oracle uses the exact fp32 values of the dequantised
+    weights (s * (q - 8) has at most 15 significant bits)."""
+    wl = WORKLOADS["c5"]
+    sh = wl.shape
+    cases = [(0, 1), (0, 4), (0, 16), (0, 64), (23, 16)]
+    cache = {}
+    for layer, B in cases:
+        d = _workload_inputs("c5", B, seed=1, layer=layer)
+        if layer not in cache:
+            cache.clear()
+            from paper_2608_15018_amd.pipeline import weights_to_device
+            ex = d["experts"]
+            deq = {n: np.stack([oracle.dequant_q4g32(ex[n][e], ex[n + "_s"][e]).astype(np.float32)
+                                for e in range(sh.n_experts)])
+                   for n in ("gate", "up", "down")}
+            cache[layer] = (weights_to_device(ex, {}), deq)
+        dw, deq = cache[layer]
+        log(f"[parity] c5 layer={layer} B={B}")
+        got, _ = run_gpu(sh, d, dw)
+        ref = oracle.forward(d["x"], d["router"], d["conf_w"], deq, {}, sh.with_(wdt="f32"))
+        check_routing(got, ref, f"c5 l={layer} B={B}")
+        errs = check_outputs(got, ref, "q4g32", f"c5 l={layer} B={B}")
+        log(f"[parity] c5 layer={layer} B={B} ok n_uniq={got['n_uniq']} errs={errs}")
