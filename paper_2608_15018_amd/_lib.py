@@ -14,7 +14,10 @@ import re
 
 import torch
 
-LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libs2moe.so")
+# S2MOE_LIBRARY may name another build of the same library (e.g. one built
+# with different tuning constants).
+LIB_PATH = os.environ.get("S2MOE_LIBRARY") or os.path.join(
+    os.path.dirname(os.path.abspath(__file__)), "libs2moe.so")
 HEADER_PATH = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
                            "include", "s2moe.h")
 

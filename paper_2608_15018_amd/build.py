@@ -17,7 +17,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 OBJDIR = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libs2moe.so")
-SOURCES = ["api.cpp", "route.hip", "gate.hip", "ffn.hip", "combine.hip"]
+SOURCES = ["api.cpp", "route.hip", "gate.hip", "ffn.hip", "ffn_bf16.hip", "combine.hip"]
 ARCH = "gfx950"
 ROCM_INC = os.path.join(os.environ.get("ROCM_PATH", "/opt/rocm"), "include")
 
@@ -28,9 +28,9 @@ COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-I", INCLUDE,
           "-Wall", "-Wno-unused-function"]
 
 
-def _compile(src: str) -> str:
-    out = os.path.join(OBJDIR, os.path.splitext(src)[0] + ".o")
-    cmd = [HIPCC, *COMMON, *DEVICE_FLAGS, "-c", os.path.join(CSRC, src), "-o", out]
+def _compile(src: str, objdir: str = OBJDIR, defines=()) -> str:
+    out = os.path.join(objdir, os.path.splitext(src)[0] + ".o")
+    cmd = [HIPCC, *COMMON, *DEVICE_FLAGS, *defines, "-c", os.path.join(CSRC, src), "-o", out]
     if src.endswith(".cpp"):
         cmd = [HIPCC, *COMMON, "-x", "c++", "-D__HIP_PLATFORM_AMD__=1", "-I", ROCM_INC, "-c",
                os.path.join(CSRC, src), "-o", out]
@@ -44,20 +44,21 @@ def _compile(src: str) -> str:
     return out
 
 
-def build(verbose: bool = True) -> str:
-    """Compile every source and link libs2moe.so; returns its path."""
-    os.makedirs(OBJDIR, exist_ok=True)
+def build(verbose: bool = True, out: str = LIB, objdir: str = OBJDIR, defines=()) -> str:
+    """Compile every source and link libs2moe.so; returns its path.  `defines`
+    (e.g. ["-DS2MOE_STAGE_STEPS=8"]) override tuning constants."""
+    os.makedirs(objdir, exist_ok=True)
     with ThreadPoolExecutor(min(len(SOURCES), os.cpu_count() or 1)) as ex:
-        objs = list(ex.map(_compile, SOURCES))
-    tmp = LIB + ".tmp"
+        objs = list(ex.map(lambda src: _compile(src, objdir, list(defines)), SOURCES))
+    tmp = out + ".tmp"
     cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{' '.join(cmd)}\n{r.stdout}{r.stderr}")
-    os.replace(tmp, LIB)
+    os.replace(tmp, out)
     if verbose:
-        print(f"built {LIB}")
-    return LIB
+        print(f"built {out}")
+    return out
 
 
 if __name__ == "__main__":

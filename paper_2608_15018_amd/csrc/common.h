@@ -83,43 +83,57 @@ __device__ __forceinline__ uint64_t lanemask_lt() {
   return lane == 0 ? 0ull : (~0ull >> (64 - lane));
 }
 
-// Wave-cooperative top-n selection over up to 256 values held four per lane
-// (value j of a lane is expert lane + 64 j).  Order: value descending, then
-// expert id ascending.  `n_sel` rounds pick the n_sel best; the experts of
-// the first `n_mark` rounds are flagged in `taken_bits` (bit j of a lane).
-// The values picked in the first and in the last round are returned
-// (wave-uniform).
-__device__ __forceinline__ void wave_topn(const float v[4], int E, int n_sel, int n_mark,
-                                          uint32_t* taken_bits, float* first_val,
-                                          float* last_val) {
-  const int lane = threadIdx.x & (kWave - 1);
-  uint64_t key[4];
+// Wave-wide reductions through DPP lane moves (quad permutes, row mirrors,
+// row broadcasts), finished by reading lane 63.  The combination order is
+// fixed, so results are deterministic.
+#define S2MOE_DPP_STEP(v, ident, op, ctrl, rmask)                                              \
+  v = op(v, __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(ident), __float_as_int(v), \
+                                                        ctrl, rmask, 0xF, false)))
+
+__device__ __forceinline__ float add_f(float a, float b) { return a + b; }
+__device__ __forceinline__ float max_f(float a, float b) { return fmaxf(a, b); }
+
+__device__ __forceinline__ float wave_sum_dpp(float v) {
+  S2MOE_DPP_STEP(v, 0.f, add_f, 0xB1, 0xF);   // quad_perm [1,0,3,2]
+  S2MOE_DPP_STEP(v, 0.f, add_f, 0x4E, 0xF);   // quad_perm [2,3,0,1]
+  S2MOE_DPP_STEP(v, 0.f, add_f, 0x141, 0xF);  // row_half_mirror
+  S2MOE_DPP_STEP(v, 0.f, add_f, 0x140, 0xF);  // row_mirror
+  S2MOE_DPP_STEP(v, 0.f, add_f, 0x142, 0xA);  // row_bcast:15
+  S2MOE_DPP_STEP(v, 0.f, add_f, 0x143, 0xC);  // row_bcast:31
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
+}
+
+__device__ __forceinline__ float wave_max_dpp(float v) {
+  const float ni = -INFINITY;
+  S2MOE_DPP_STEP(v, ni, max_f, 0xB1, 0xF);
+  S2MOE_DPP_STEP(v, ni, max_f, 0x4E, 0xF);
+  S2MOE_DPP_STEP(v, ni, max_f, 0x141, 0xF);
+  S2MOE_DPP_STEP(v, ni, max_f, 0x140, 0xF);
+  S2MOE_DPP_STEP(v, ni, max_f, 0x142, 0xA);
+  S2MOE_DPP_STEP(v, ni, max_f, 0x143, 0xC);
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
+}
+
+// 48-bit ranking key of expert e with value v: value descending first, then
+// expert id ascending.  0 marks an empty slot (below every real key).
+__device__ __forceinline__ uint64_t rank_key(float v, int e) {
+  return ((uint64_t)order_key(v) << 16) | (uint32_t)(0xFFFF - e);
+}
+
+// The k-th largest of the distinct keys held four per lane (bit-by-bit
+// search of the threshold: ballots count the keys at or above a candidate).
+// Exactly k keys are >= the result.  Wave-uniform.
+__device__ __forceinline__ uint64_t wave_kth_key(const uint64_t key[4], int nj, int k) {
+  uint64_t prefix = 0;
+  for (int bit = 47; bit >= 0; --bit) {
+    const uint64_t cand = prefix | (1ull << bit);
+    int cnt = 0;
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int e = lane + kWave * j;
-    key[j] = (e < E) ? (((uint64_t)order_key(v[j]) << 32) | (uint32_t)(0xFFFFu - e)) : 0ull;
+    for (int j = 0; j < 4; ++j)
+      if (j < nj) cnt += __popcll(__ballot(key[j] >= cand));
+    if (cnt >= k) prefix = cand;
   }
-  uint32_t bits = 0;
-  float first = 0.f, last = 0.f;
-  for (int r = 0; r < n_sel; ++r) {
-    uint64_t best = key[0];
-#pragma unroll
-    for (int j = 1; j < 4; ++j) best = key[j] > best ? key[j] : best;
-    best = wave_max_u64(best);
-    const int e = 0xFFFF - (int)(uint32_t)(best & 0xFFFFu);
-    last = key_value((uint32_t)(best >> 32));
-    if (r == 0) first = last;
-    if ((e & (kWave - 1)) == lane) {
-      const int j = e / kWave;
-#pragma unroll
-      for (int jj = 0; jj < 4; ++jj)
-        if (jj == j) key[jj] = 0ull;
-      if (r < n_mark) bits |= 1u << j;
-    }
-  }
-  *taken_bits = bits;
-  *first_val = first;
-  *last_val = last;
+  return prefix;
 }
 
 // Rank, in ascending expert id, of the flagged experts: expert lane + 64 j

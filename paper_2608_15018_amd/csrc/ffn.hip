@@ -22,71 +22,13 @@
 // P = sum (128 + q) x and a second MFMA with an all-ones A gives Sx = sum x,
 // and the group contributes s * (P - 136 Sx) = s * sum (q - 8) x in fp32.
 // No dequantised weight ever reaches memory.
-#include "common.h"
-#include "kernels.h"
+#include "ffn_common.h"
 
 namespace s2moe {
 
+using namespace ffn;
+
 namespace {
-
-struct Segment {
-  int n;      // tokens
-  int base;   // routed: offset[e] (row of its first token in Hh); shared: B*k + s*B
-  int id;     // expert e or shared expert s
-  bool shared;
-};
-
-// Grid layout: shared-expert blocks first (always live), then routed blocks
-// u-major (u = position in uniq), so blocks of inactive experts come last
-// and exit at once.
-__device__ __forceinline__ bool resolve_block(const FfnArgs& a, int mode, int rows_per_block,
-                                              Segment* seg, int* rb) {
-  const int rows_r = mode == 0 ? a.F : a.H;
-  const int rows_s = mode == 0 ? a.Fs : a.H;
-  const int nbs = a.S > 0 ? rows_s / rows_per_block : 0;
-  const int nbr = rows_r / rows_per_block;
-  int bid = blockIdx.x;
-  if (bid < a.S * nbs) {
-    seg->shared = true;
-    seg->id = bid / nbs;
-    *rb = bid % nbs;
-    seg->n = a.B;
-    seg->base = a.B * a.k + seg->id * a.B;
-    return true;
-  }
-  bid -= a.S * nbs;
-  const int u = bid / nbr;
-  *rb = bid % nbr;
-  if (u >= min(*a.n_uniq, a.E)) return false;
-  // The routing arrays come from the gating step; values outside their
-  // ranges (routing never computed) make the block idle instead of faulting.
-  const int e = a.uniq[u];
-  if (e < 0 || e >= a.E) return false;
-  seg->shared = false;
-  seg->id = e;
-  seg->n = a.count[e];
-  seg->base = a.offset[e];
-  return seg->n > 0 && seg->base >= 0 && seg->base + seg->n <= a.B * a.k;
-}
-
-__device__ __forceinline__ int slot_at(const FfnArgs& a, int i) {
-  const int v = a.slot[i];
-  return min(max(v, 0), a.B * a.k - 1);
-}
-
-// Row of the X source feeding token t of the segment: x for gate-up
-// (gathered through slot), the segment's own Hh rows for down.
-__device__ __forceinline__ int x_row(const FfnArgs& a, int mode, const Segment& s, int t) {
-  if (mode == 0) return s.shared ? t : slot_at(a, s.base + t) / a.k;
-  return s.base + t;
-}
-
-// Row of expert_out written for token t (down only).
-__device__ __forceinline__ int out_row(const FfnArgs& a, const Segment& s, int t) {
-  return s.shared ? s.base + t : slot_at(a, s.base + t);
-}
-
-__device__ __forceinline__ float silu(float z) { return z / (1.f + expf(-z)); }
 
 // ---------------------------------------------------------------- fp32 path
 template <int kMode>
@@ -151,103 +93,6 @@ __global__ __launch_bounds__(256) void ffn_f32_kernel(FfnArgs a) {
         else
           a.out[(size_t)out_row(a, seg, t) * a.H + row] = acc0[tt];
       }
-    }
-  }
-}
-
-// ---------------------------------------------------------------- MFMA path
-__device__ __forceinline__ f32x4 mfma(bf16x8 a, bf16x8 b, f32x4 c) {
-  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
-}
-
-__device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) {
-  bf16x8 r;
-  __builtin_memcpy(&r, &v, 16);
-  return r;
-}
-
-// 8 codes of one dword -> the bf16 values 128 + q, in the element order
-// (0, 4, 2, 6, 1, 5, 3, 7) of K offsets within the lane's 8.
-__device__ __forceinline__ bf16x8 q4_expand(uint32_t w) {
-  u32x4 d;
-  d[0] = (w & 0x000F000Fu) | 0x43004300u;
-  d[1] = ((w >> 8) & 0x000F000Fu) | 0x43004300u;
-  d[2] = ((w >> 4) & 0x000F000Fu) | 0x43004300u;
-  d[3] = ((w >> 12) & 0x000F000Fu) | 0x43004300u;
-  return as_bf16x8(d);
-}
-
-// Natural-order activations (k0..k7) -> the element order of q4_expand.
-__device__ __forceinline__ bf16x8 q4_permute_x(u32x4 x) {
-  u32x4 d;
-  d[0] = (x[0] & 0xFFFFu) | (x[2] << 16);          // k0, k4
-  d[1] = (x[1] & 0xFFFFu) | (x[3] << 16);          // k2, k6
-  d[2] = (x[0] >> 16) | (x[2] & 0xFFFF0000u);      // k1, k5
-  d[3] = (x[1] >> 16) | (x[3] & 0xFFFF0000u);      // k3, k7
-  return as_bf16x8(d);
-}
-
-template <int T, int kMode, int U>
-__device__ __forceinline__ void mfma_tile_bf16(const FfnArgs& a, const Segment& seg, int t0,
-                                               int r0, int K, const uint16_t* W0,
-                                               const uint16_t* W1) {
-  constexpr bool kDual = kMode == 0;
-  const int lane = threadIdx.x & (kWave - 1);
-  const int rA = lane & 15, gK = lane >> 4;
-  const int nks = K / 32;
-  const uint16_t* X = static_cast<const uint16_t*>(kMode == 0 ? a.x : a.hh);
-  const int ldx = kMode == 0 ? a.H : a.ldh;
-  const u32x4* xb[T];
-#pragma unroll
-  for (int tt = 0; tt < T; ++tt) {
-    const int t = min(t0 + tt * 16 + rA, seg.n - 1);
-    xb[tt] = reinterpret_cast<const u32x4*>(X + (size_t)x_row(a, kMode, seg, t) * ldx) + gK;
-  }
-  const u32x4* pa0 = reinterpret_cast<const u32x4*>(W0 + (size_t)(r0 + rA) * K) + gK;
-  const u32x4* pa1 = kDual ? reinterpret_cast<const u32x4*>(W1 + (size_t)(r0 + rA) * K) + gK
-                           : pa0;
-  f32x4 acc0[T], acc1[T];
-#pragma unroll
-  for (int tt = 0; tt < T; ++tt) {
-    acc0[tt] = f32x4{0.f, 0.f, 0.f, 0.f};
-    acc1[tt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  }
-  for (int ks = 0; ks < nks; ks += U) {
-    u32x4 A0[U], A1[U], Bf[T][U];
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      A0[u] = pa0[4 * (ks + u)];
-      if (kDual) A1[u] = pa1[4 * (ks + u)];
-    }
-#pragma unroll
-    for (int tt = 0; tt < T; ++tt)
-#pragma unroll
-      for (int u = 0; u < U; ++u) Bf[tt][u] = xb[tt][4 * (ks + u)];
-#pragma unroll
-    for (int u = 0; u < U; ++u)
-#pragma unroll
-      for (int tt = 0; tt < T; ++tt) {
-        acc0[tt] = mfma(as_bf16x8(A0[u]), as_bf16x8(Bf[tt][u]), acc0[tt]);
-        if (kDual) acc1[tt] = mfma(as_bf16x8(A1[u]), as_bf16x8(Bf[tt][u]), acc1[tt]);
-      }
-  }
-  // Epilogue.  Lane holds D[m][n] for token n = rA, rows m = 4 gK + i.
-  const int m0 = r0 + 4 * gK;
-#pragma unroll
-  for (int tt = 0; tt < T; ++tt) {
-    const int t = t0 + tt * 16 + rA;
-    if (t >= seg.n) continue;
-    if (kMode == 0) {
-      uint32_t h[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) h[i] = f32_to_bf16(silu(acc0[tt][i]) * acc1[tt][i]);
-      uint2 v;
-      v.x = h[0] | (h[1] << 16);
-      v.y = h[2] | (h[3] << 16);
-      *reinterpret_cast<uint2*>(static_cast<uint16_t*>(a.hh) + (size_t)(seg.base + t) * a.ldh +
-                                m0) = v;
-    } else {
-      *reinterpret_cast<f32x4*>(a.out + (size_t)out_row(a, seg, t) * a.H + m0) = acc0[tt];
     }
   }
 }
@@ -356,8 +201,8 @@ __device__ __forceinline__ void mfma_tile_q4(const FfnArgs& a, const Segment& se
   }
 }
 
-template <int kMode, bool kQ4>
-__global__ __launch_bounds__(256) void ffn_mfma_kernel(FfnArgs a) {
+template <int kMode>
+__global__ __launch_bounds__(256) void ffn_q4_kernel(FfnArgs a) {
   Segment seg;
   int rb;
   if (!resolve_block(a, kMode, 64, &seg, &rb)) return;
@@ -380,41 +225,20 @@ __global__ __launch_bounds__(256) void ffn_mfma_kernel(FfnArgs a) {
   const size_t mat = (size_t)rows * K;  // weights per expert matrix
   for (int t0 = 0; t0 < seg.n; t0 += 64) {
     const int T = min(4, (seg.n - t0 + 15) / 16);
-    if (kQ4) {
-      const uint8_t* C0 = static_cast<const uint8_t*>(M0) + seg.id * (mat / 2);
-      const uint8_t* C1 = kMode == 0 ? static_cast<const uint8_t*>(M1) + seg.id * (mat / 2) : C0;
-      const uint16_t* S0 = static_cast<const uint16_t*>(Q0) + seg.id * (mat / 32);
-      const uint16_t* S1 =
-          kMode == 0 ? static_cast<const uint16_t*>(Q1) + seg.id * (mat / 32) : S0;
-      switch (T) {
-        case 1: mfma_tile_q4<1, kMode>(a, seg, t0, r0, K, C0, C1, S0, S1); break;
-        case 2: mfma_tile_q4<2, kMode>(a, seg, t0, r0, K, C0, C1, S0, S1); break;
-        case 3: mfma_tile_q4<3, kMode>(a, seg, t0, r0, K, C0, C1, S0, S1); break;
-        default: mfma_tile_q4<4, kMode>(a, seg, t0, r0, K, C0, C1, S0, S1); break;
-      }
-    } else {
-      const uint16_t* W0 = static_cast<const uint16_t*>(M0) + seg.id * mat;
-      const uint16_t* W1 = kMode == 0 ? static_cast<const uint16_t*>(M1) + seg.id * mat : W0;
-      const bool u8 = ((K / 32) % 8) == 0;
-      switch (T * 2 + (u8 ? 1 : 0)) {
-        case 2: mfma_tile_bf16<1, kMode, 2>(a, seg, t0, r0, K, W0, W1); break;
-        case 3: mfma_tile_bf16<1, kMode, 8>(a, seg, t0, r0, K, W0, W1); break;
-        case 4: mfma_tile_bf16<2, kMode, 2>(a, seg, t0, r0, K, W0, W1); break;
-        case 5: mfma_tile_bf16<2, kMode, 8>(a, seg, t0, r0, K, W0, W1); break;
-        case 6: mfma_tile_bf16<3, kMode, 2>(a, seg, t0, r0, K, W0, W1); break;
-        case 7: mfma_tile_bf16<3, kMode, 8>(a, seg, t0, r0, K, W0, W1); break;
-        case 8: mfma_tile_bf16<4, kMode, 2>(a, seg, t0, r0, K, W0, W1); break;
-        default: mfma_tile_bf16<4, kMode, 8>(a, seg, t0, r0, K, W0, W1); break;
-      }
+    const uint8_t* C0 = static_cast<const uint8_t*>(M0) + seg.id * (mat / 2);
+    const uint8_t* C1 = kMode == 0 ? static_cast<const uint8_t*>(M1) + seg.id * (mat / 2) : C0;
+    const uint16_t* S0 = static_cast<const uint16_t*>(Q0) + seg.id * (mat / 32);
+    const uint16_t* S1 =
+        kMode == 0 ? static_cast<const uint16_t*>(Q1) + seg.id * (mat / 32) : S0;
+    switch (T) {
+      case 1: mfma_tile_q4<1, kMode>(a, seg, t0, r0, K, C0, C1, S0, S1); break;
+      case 2: mfma_tile_q4<2, kMode>(a, seg, t0, r0, K, C0, C1, S0, S1); break;
+      case 3: mfma_tile_q4<3, kMode>(a, seg, t0, r0, K, C0, C1, S0, S1); break;
+      default: mfma_tile_q4<4, kMode>(a, seg, t0, r0, K, C0, C1, S0, S1); break;
     }
   }
 }
 
-int n_blocks(const FfnArgs& a, int mode, int rows_per_block) {
-  const int rows_r = mode == 0 ? a.F : a.H;
-  const int rows_s = mode == 0 ? a.Fs : a.H;
-  return (a.S > 0 ? a.S * (rows_s / rows_per_block) : 0) + a.E * (rows_r / rows_per_block);
-}
 
 }  // namespace
 
@@ -426,17 +250,11 @@ hipError_t launch_ffn(const FfnArgs& a, hipStream_t s) {
     hipLaunchKernelGGL(ffn_f32_kernel<1>, dim3(n_blocks(a, 1, 4)), dim3(256), 0, s, a);
     return hipGetLastError();
   }
-  if (a.wf == kWBf16) {
-    hipLaunchKernelGGL((ffn_mfma_kernel<0, false>), dim3(n_blocks(a, 0, 64)), dim3(256), 0, s, a);
-    hipError_t err = hipGetLastError();
-    if (err != hipSuccess) return err;
-    hipLaunchKernelGGL((ffn_mfma_kernel<1, false>), dim3(n_blocks(a, 1, 64)), dim3(256), 0, s, a);
-    return hipGetLastError();
-  }
-  hipLaunchKernelGGL((ffn_mfma_kernel<0, true>), dim3(n_blocks(a, 0, 64)), dim3(256), 0, s, a);
+  if (a.wf == kWBf16) return launch_ffn_bf16(a, s);
+  hipLaunchKernelGGL(ffn_q4_kernel<0>, dim3(n_blocks(a, 0, 64)), dim3(256), 0, s, a);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
-  hipLaunchKernelGGL((ffn_mfma_kernel<1, true>), dim3(n_blocks(a, 1, 64)), dim3(256), 0, s, a);
+  hipLaunchKernelGGL(ffn_q4_kernel<1>, dim3(n_blocks(a, 1, 64)), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

@@ -1,0 +1,110 @@
+// Work decomposition shared by the expert-FFN kernels.
+#pragma once
+
+#include "common.h"
+#include "kernels.h"
+
+namespace s2moe {
+namespace ffn {
+
+struct Segment {
+  int n;      // tokens
+  int base;   // routed: offset[e] (row of its first token in Hh); shared: B*k + s*B
+  int id;     // expert e or shared expert s
+  bool shared;
+};
+
+// Grid layout: shared-expert blocks first (always live), then routed blocks
+// u-major (u = position in uniq), so blocks of inactive experts come last
+// and exit at once.
+__device__ __forceinline__ bool resolve_block(const FfnArgs& a, int mode, int rows_per_block,
+                                              Segment* seg, int* rb) {
+  const int rows_r = mode == 0 ? a.F : a.H;
+  const int rows_s = mode == 0 ? a.Fs : a.H;
+  const int nbs = a.S > 0 ? rows_s / rows_per_block : 0;
+  const int nbr = rows_r / rows_per_block;
+  int bid = blockIdx.x;
+  if (bid < a.S * nbs) {
+    seg->shared = true;
+    seg->id = bid / nbs;
+    *rb = bid % nbs;
+    seg->n = a.B;
+    seg->base = a.B * a.k + seg->id * a.B;
+    return true;
+  }
+  bid -= a.S * nbs;
+  const int u = bid / nbr;
+  *rb = bid % nbr;
+  if (u >= min(*a.n_uniq, a.E)) return false;
+  // The routing arrays come from the gating step; values outside their
+  // ranges (routing never computed) make the block idle instead of faulting.
+  const int e = a.uniq[u];
+  if (e < 0 || e >= a.E) return false;
+  seg->shared = false;
+  seg->id = e;
+  seg->n = a.count[e];
+  seg->base = a.offset[e];
+  return seg->n > 0 && seg->base >= 0 && seg->base + seg->n <= a.B * a.k;
+}
+
+__device__ __forceinline__ int slot_at(const FfnArgs& a, int i) {
+  const int v = a.slot[i];
+  return min(max(v, 0), a.B * a.k - 1);
+}
+
+// Row of the X source feeding token t of the segment: x for gate-up
+// (gathered through slot), the segment's own Hh rows for down.
+__device__ __forceinline__ int x_row(const FfnArgs& a, int mode, const Segment& s, int t) {
+  if (mode == 0) return s.shared ? t : slot_at(a, s.base + t) / a.k;
+  return s.base + t;
+}
+
+// Row of expert_out written for token t (down only).
+__device__ __forceinline__ int out_row(const FfnArgs& a, const Segment& s, int t) {
+  return s.shared ? s.base + t : slot_at(a, s.base + t);
+}
+
+__device__ __forceinline__ float silu(float z) { return z / (1.f + expf(-z)); }
+
+// MFMA helpers.
+__device__ __forceinline__ f32x4 mfma(bf16x8 a, bf16x8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) {
+  bf16x8 r;
+  __builtin_memcpy(&r, &v, 16);
+  return r;
+}
+
+// 8 codes of one dword -> the bf16 values 128 + q, in the element order
+// (0, 4, 2, 6, 1, 5, 3, 7) of K offsets within the lane's 8.
+__device__ __forceinline__ bf16x8 q4_expand(uint32_t w) {
+  u32x4 d;
+  d[0] = (w & 0x000F000Fu) | 0x43004300u;
+  d[1] = ((w >> 8) & 0x000F000Fu) | 0x43004300u;
+  d[2] = ((w >> 4) & 0x000F000Fu) | 0x43004300u;
+  d[3] = ((w >> 12) & 0x000F000Fu) | 0x43004300u;
+  return as_bf16x8(d);
+}
+
+// Natural-order activations (k0..k7) -> the element order of q4_expand.
+__device__ __forceinline__ bf16x8 q4_permute_x(u32x4 x) {
+  u32x4 d;
+  d[0] = (x[0] & 0xFFFFu) | (x[2] << 16);          // k0, k4
+  d[1] = (x[1] & 0xFFFFu) | (x[3] << 16);          // k2, k6
+  d[2] = (x[0] >> 16) | (x[2] & 0xFFFF0000u);      // k1, k5
+  d[3] = (x[1] >> 16) | (x[3] & 0xFFFF0000u);      // k3, k7
+  return as_bf16x8(d);
+}
+
+
+// Number of blocks of `rows_per_block` rows over all experts a launch covers.
+inline int n_blocks(const FfnArgs& a, int mode, int rows_per_block) {
+  const int rows_r = mode == 0 ? a.F : a.H;
+  const int rows_s = mode == 0 ? a.Fs : a.H;
+  return (a.S > 0 ? a.S * (rows_s / rows_per_block) : 0) + a.E * (rows_r / rows_per_block);
+}
+
+}  // namespace ffn
+}  // namespace s2moe

@@ -3,68 +3,85 @@
 // preferred expert selection, soft routing bias for reuse promotion).
 //
 // One workgroup of 16 waves handles the whole verify batch (B <= 256,
-// E <= 256): the gating decisions couple all tokens through g, and the
-// batch is small enough that one CU finishes it in a few microseconds.
-// Every result is deterministic: integer LDS atomics only, fixed-order
-// floating-point sums, rank-based (not atomic-order-based) placement.
+// E <= 256): the decisions couple all tokens through g, and the batch is
+// small.  Nothing here is a serial loop over assignments:
+//   * g: one thread per expert sums w_b * ell_{b,e} over b in order;
+//   * TopCap: each expert's rank among the candidates by (g desc, id asc);
+//   * per token (one wave): biased keys, a bitwise threshold search for the
+//     k-th largest key, ballot ranks for ascending-id order, DPP softmax;
+//   * buckets: a B-bit token mask per expert (LDS 64-bit ORs), so an
+//     assignment's position in its expert's list is the popcount of the mask
+//     below its token.
+// Every result is deterministic: integer atomics only (bitwise OR), fixed
+// floating-point summation orders, rank-based placement.
 #include "common.h"
 #include "kernels.h"
 
 namespace s2moe {
 
 __global__ __launch_bounds__(1024) void reuse_gate_kernel(GateArgs a) {
+  constexpr int kMaskWords = kMaxTokens / 64;
+  constexpr int kStage = 10240;  // logits staged in LDS up to B * E = 10240
+  __shared__ float ell_s[kStage];
   __shared__ float w_s[kMaxTokens];
-  __shared__ float g_s[kMaxExperts];
-  __shared__ int cand_s[kMaxExperts];
+  __shared__ float gm_s[kMaxExperts];  // g of candidates, -inf otherwise
   __shared__ int pref_s[kMaxExperts];
   __shared__ int count_s[kMaxExperts];
   __shared__ int offset_s[kMaxExperts + 1];
+  __shared__ uint64_t mask_s[kMaxExperts][kMaskWords];
   __shared__ uint8_t idx_s[kMaxTokens * kMaxTopK];
+  __shared__ int cand_s[kMaxExperts];
 
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
   const int wave = tid >> 6;
   const int n_waves = blockDim.x >> 6;
   const int B = a.B, E = a.E, k = a.k;
+  const bool staged = B * E <= kStage;
 
-  // Non-negative confidence weights w_b.
+  // Non-negative confidences w_b; logits to LDS; cleared masks.
   int positive = 0;
   if (tid < B) {
     const float w = fmaxf(a.conf_w[tid], 0.f);
     w_s[tid] = w;
     positive = w > 0.f;
   }
-  if (tid < kMaxExperts) {
-    cand_s[tid] = (!(a.flags & kPrefActivatedOnly) && tid < E) ? 1 : 0;
-    count_s[tid] = 0;
-  }
+  if (staged)
+    for (int i = tid; i < B * E; i += blockDim.x) ell_s[i] = a.logits[i];
+  for (int i = tid; i < kMaxExperts * kMaskWords; i += blockDim.x)
+    (&mask_s[0][0])[i] = 0ull;
+  if (tid < kMaxExperts) cand_s[tid] = (!(a.flags & kPrefActivatedOnly) && tid < E) ? 1 : 0;
   const int active = __syncthreads_or(positive);
+  const float* ell = staged ? ell_s : a.logits;
 
   // TopCap candidates: all experts, or those in some token's plain top-k.
-  if (a.flags & kPrefActivatedOnly)
+  if (a.flags & kPrefActivatedOnly) {
     for (int i = tid; i < B * k; i += blockDim.x) {
       const int e = a.plain_idx[i];
       if (e >= 0 && e < E) cand_s[e] = 1;
     }
+    __syncthreads();
+  }
 
   // g_e = sum_b w_b * ell_{b,e}, summed over b in order.
   if (tid < E) {
     float s = 0.f;
-    for (int b = 0; b < B; ++b) s = fmaf(w_s[b], a.logits[(size_t)b * E + tid], s);
-    g_s[tid] = s;
+#pragma unroll 8
+    for (int b = 0; b < B; ++b) s = fmaf(w_s[b], ell[(size_t)b * E + tid], s);
     a.g[tid] = s;
+    gm_s[tid] = cand_s[tid] ? s : -INFINITY;
   }
   __syncthreads();
 
-  // E* = TopCap(g): rank of e among candidates by (g desc, id asc).
+  // E* = TopCap(g): rank of each candidate by (g desc, id asc).
   if (tid < E) {
     int p = 0;
     if (active && cand_s[tid]) {
-      const float ge = g_s[tid];
+      const float ge = gm_s[tid];
       int rank = 0;
+#pragma unroll 8
       for (int e2 = 0; e2 < E; ++e2) {
-        if (!cand_s[e2]) continue;
-        const float g2 = g_s[e2];
+        const float g2 = gm_s[e2];
         rank += (g2 > ge) || (g2 == ge && e2 < tid);
       }
       p = rank < a.cap;
@@ -74,29 +91,39 @@ __global__ __launch_bounds__(1024) void reuse_gate_kernel(GateArgs a) {
   }
   __syncthreads();
 
-  // Per token: lambda_b, biased logits, biased top-k, gate weights.
+  // Per token: lambda_b, biased keys, biased top-k, gate weights, masks.
+  const int nj = (E + kWave - 1) / kWave;
+  const bool from_biased = (a.flags & kGateFromBiased) != 0;
   for (int b = wave; b < B; b += n_waves) {
     float lam = 0.f;
     if (active) lam = (a.flags & kBiasAbsolute) ? a.alpha : a.alpha * a.gap[b];
     float l[4], lb[4];
+    uint64_t key[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int e = lane + kWave * j;
-      l[j] = e < E ? a.logits[(size_t)b * E + e] : 0.f;
-      lb[j] = (e < E && pref_s[e]) ? l[j] + lam : l[j];
+      l[j] = 0.f;
+      lb[j] = 0.f;
+      key[j] = 0;
+      if (e < E) {
+        l[j] = ell[(size_t)b * E + e];
+        lb[j] = pref_s[e] ? l[j] + lam : l[j];
+        key[j] = rank_key(lb[j], e);
+      }
     }
-    uint32_t bits;
-    float first, last;
-    wave_topn(lb, E, k, k, &bits, &first, &last);
-    int rank[4];
-    wave_rank_flagged(bits, rank);
-
-    const bool from_biased = (a.flags & kGateFromBiased) != 0;
+    const uint64_t kth = wave_kth_key(key, nj, k);
+    uint32_t bits = 0;
     float m = -INFINITY;
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
-      if ((bits >> j) & 1u) m = fmaxf(m, from_biased ? lb[j] : l[j]);
-    m = wave_max(m);
+    for (int j = 0; j < 4; ++j) {
+      if (key[j] != 0 && key[j] >= kth) {
+        bits |= 1u << j;
+        m = fmaxf(m, from_biased ? lb[j] : l[j]);
+      }
+    }
+    int rank[4];
+    wave_rank_flagged(bits, rank);
+    m = wave_max_dpp(m);
     float ez[4];
     float s = 0.f;
 #pragma unroll
@@ -104,7 +131,7 @@ __global__ __launch_bounds__(1024) void reuse_gate_kernel(GateArgs a) {
       ez[j] = ((bits >> j) & 1u) ? expf((from_biased ? lb[j] : l[j]) - m) : 0.f;
       s += ez[j];
     }
-    s = wave_sum(s);
+    s = wave_sum_dpp(s);
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       if ((bits >> j) & 1u) {
@@ -113,13 +140,21 @@ __global__ __launch_bounds__(1024) void reuse_gate_kernel(GateArgs a) {
         a.idx[pos] = e;
         a.gate_w[pos] = ez[j] / s;
         idx_s[pos] = (uint8_t)e;
+        atomicOr(reinterpret_cast<unsigned long long*>(&mask_s[e][b >> 6]),
+                 1ull << (b & 63));
       }
     }
   }
   __syncthreads();
 
-  // Bucketing: counts, exclusive offsets, activated experts.
-  for (int i = tid; i < B * k; i += blockDim.x) atomicAdd(&count_s[idx_s[i]], 1);
+  // Counts from the masks; exclusive offsets and the activated-expert list.
+  if (tid < E) {
+    int c = 0;
+#pragma unroll
+    for (int w = 0; w < kMaskWords; ++w) c += __popcll(mask_s[tid][w]);
+    count_s[tid] = c;
+    a.count[tid] = c;
+  }
   __syncthreads();
   if (wave == 0) {
     int c[4], f[4], sum_c = 0, sum_f = 0;
@@ -139,6 +174,7 @@ __global__ __launch_bounds__(1024) void reuse_gate_kernel(GateArgs a) {
       const int e = lane * 4 + j;
       if (e < E) {
         offset_s[e] = run_c;
+        a.offset[e] = run_c;
         if (f[j]) a.uniq[run_f] = e;
       }
       run_c += c[j];
@@ -147,23 +183,26 @@ __global__ __launch_bounds__(1024) void reuse_gate_kernel(GateArgs a) {
     for (int i = total_f + lane; i < E; i += kWave) a.uniq[i] = -1;
     if (lane == 0) {
       offset_s[E] = total_c;
+      a.offset[E] = total_c;
       *a.n_uniq = total_f;
     }
   }
   __syncthreads();
 
-  // Stable expert-major slot list: expert e lists its assignments a = b*k+j
-  // in increasing a.
-  if (tid < E) {
-    int p = offset_s[tid];
-    const int c = count_s[tid];
-    a.count[tid] = c;
-    a.offset[tid] = p;
-    if (c > 0)
-      for (int i = 0; i < B * k; ++i)
-        if (idx_s[i] == tid) a.slot[p++] = i;
+  // Stable expert-major slot list: assignment (b, j) of expert e goes after
+  // the assignments of e by tokens b' < b.
+  for (int i = tid; i < B * k; i += blockDim.x) {
+    const int b = i / k;
+    const int e = idx_s[i];
+    int before = 0;
+#pragma unroll
+    for (int w = 0; w < kMaskWords; ++w) {
+      const uint64_t m = mask_s[e][w];
+      if (w < (b >> 6)) before += __popcll(m);
+      else if (w == (b >> 6)) before += __popcll(m & ((1ull << (b & 63)) - 1ull));
+    }
+    a.slot[offset_s[e] + before] = i;
   }
-  if (tid == 0) a.offset[E] = offset_s[E];
 }
 
 hipError_t launch_reuse_gate(const GateArgs& a, hipStream_t s) {

@@ -74,6 +74,7 @@ struct CombineArgs {
 hipError_t launch_route(const RouteArgs& a, hipStream_t s);
 hipError_t launch_reuse_gate(const GateArgs& a, hipStream_t s);
 hipError_t launch_ffn(const FfnArgs& a, hipStream_t s);
+hipError_t launch_ffn_bf16(const FfnArgs& a, hipStream_t s);
 hipError_t launch_combine(const CombineArgs& a, hipStream_t s);
 
 }  // namespace s2moe
