@@ -77,28 +77,6 @@ __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) {
   return r;
 }
 
-// 8 codes of one dword -> the bf16 values 128 + q, in the element order
-// (0, 4, 2, 6, 1, 5, 3, 7) of K offsets within the lane's 8.
-__device__ __forceinline__ bf16x8 q4_expand(uint32_t w) {
-  u32x4 d;
-  d[0] = (w & 0x000F000Fu) | 0x43004300u;
-  d[1] = ((w >> 8) & 0x000F000Fu) | 0x43004300u;
-  d[2] = ((w >> 4) & 0x000F000Fu) | 0x43004300u;
-  d[3] = ((w >> 12) & 0x000F000Fu) | 0x43004300u;
-  return as_bf16x8(d);
-}
-
-// Natural-order activations (k0..k7) -> the element order of q4_expand.
-__device__ __forceinline__ bf16x8 q4_permute_x(u32x4 x) {
-  u32x4 d;
-  d[0] = (x[0] & 0xFFFFu) | (x[2] << 16);          // k0, k4
-  d[1] = (x[1] & 0xFFFFu) | (x[3] << 16);          // k2, k6
-  d[2] = (x[0] >> 16) | (x[2] & 0xFFFF0000u);      // k1, k5
-  d[3] = (x[1] >> 16) | (x[3] & 0xFFFF0000u);      // k3, k7
-  return as_bf16x8(d);
-}
-
-
 // Number of blocks of `rows_per_block` rows over all experts a launch covers.
 inline int n_blocks(const FfnArgs& a, int mode, int rows_per_block) {
   const int rows_r = mode == 0 ? a.F : a.H;

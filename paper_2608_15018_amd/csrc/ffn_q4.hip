@@ -1,0 +1,319 @@
+// int4 expert FFN (4-bit codes, one fp16 scale per 32 K elements) on the
+// matrix cores, decoding inside the weight stream.
+//
+// A lane reads one whole 32-code group (16 bytes) of its weight row per
+// 128-wide "super-step" (lanes 16 apart take consecutive groups, so a row's
+// 64 bytes arrive in one load) plus that group's scale.  Each code dword
+// (8 codes) becomes the fp16 values 1024 + q with one and-or per pair; a
+// packed add of -1032 gives q - 8 exactly, and a packed multiply by the
+// group scale gives round_fp16(s * (q - 8)).  The four dwords are the A
+// operands of four v_mfma_f32_16x16x32_f16, accumulated in fp32, so no
+// dequantised weight is ever written to memory and no per-group epilogue is
+// needed.  The expansion yields the K order (0,4,2,6,1,5,3,7) inside each
+// 8-element block; the activations are kept in fp16 in that same order (a
+// prep kernel converts x, the gate-up epilogue writes Hh so), so the B
+// operands are plain 16-byte loads.
+//
+// Work decomposition as in the bf16 kernel: R 16-row tiles per unit, W waves
+// split K, double-buffered register pipeline, LDS reduction in wave order.
+#include "ffn_common.h"
+
+namespace s2moe {
+
+using namespace ffn;
+
+namespace {
+
+typedef _Float16 half2v __attribute__((ext_vector_type(2)));
+typedef _Float16 half8v __attribute__((ext_vector_type(8)));
+
+__device__ __forceinline__ f32x4 mfma16(half8v a, half8v b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ half8v as_half8(u32x4 v) {
+  half8v r;
+  __builtin_memcpy(&r, &v, 16);
+  return r;
+}
+
+// Position of element e of an 8-element block in the expansion order
+// (0,4,2,6,1,5,3,7); the order is its own inverse.
+__device__ __forceinline__ int perm8(int e) {
+  return ((e & 1) << 2) | (e & 2) | ((e >> 2) & 1);
+}
+
+// 8 codes (one dword) -> s * (q - 8) as fp16, in expansion order.
+__device__ __forceinline__ half8v q4_decode(uint32_t w, half2v s2) {
+  const half2v off = {(_Float16)-1032.0f, (_Float16)-1032.0f};
+  uint32_t d[4];
+  d[0] = (w & 0x000F000Fu) | 0x64006400u;
+  d[1] = ((w >> 8) & 0x000F000Fu) | 0x64006400u;
+  d[2] = ((w >> 4) & 0x000F000Fu) | 0x64006400u;
+  d[3] = ((w >> 12) & 0x000F000Fu) | 0x64006400u;
+  half8v r;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    half2v h;
+    __builtin_memcpy(&h, &d[i], 4);
+    h = (h + off) * s2;
+    r[2 * i] = h[0];
+    r[2 * i + 1] = h[1];
+  }
+  return r;
+}
+
+template <int T, int R, int NM>
+struct StageQ {
+  u32x4 c[NM][R];     // one 32-code group per lane
+  uint32_t s[NM][R];  // its fp16 scale (low half)
+  u32x4 b[T][4];      // 4 x 8 activations per token tile
+};
+
+template <int T, int R, int NM>
+__device__ __forceinline__ void load_q(StageQ<T, R, NM>& st, const u32x4* const* pc,
+                                       const uint16_t* const* ps, const u32x4* const* xb,
+                                       int s, int hi) {
+  s = min(s, hi - 1);
+#pragma unroll
+  for (int m = 0; m < NM; ++m)
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      st.c[m][r] = pc[m * R + r][4 * s];
+      st.s[m][r] = ps[m * R + r][4 * s];
+    }
+#pragma unroll
+  for (int tt = 0; tt < T; ++tt)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) st.b[tt][j] = xb[tt][16 * s + j];
+}
+
+template <int T, int R, int NM>
+__device__ __forceinline__ void compute_q(const StageQ<T, R, NM>& st, f32x4 (&acc)[NM][R][T],
+                                          int s, int hi) {
+  if (s >= hi) return;
+#pragma unroll
+  for (int m = 0; m < NM; ++m)
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      _Float16 sh;
+      const uint16_t bits = (uint16_t)st.s[m][r];
+      __builtin_memcpy(&sh, &bits, 2);
+      const half2v s2 = {sh, sh};
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const half8v a = q4_decode(st.c[m][r][j], s2);
+#pragma unroll
+        for (int tt = 0; tt < T; ++tt)
+          acc[m][r][tt] = mfma16(a, as_half8(st.b[tt][j]), acc[m][r][tt]);
+      }
+    }
+}
+
+template <int kMode, int T, int TMAX, int R, int W>
+__device__ __forceinline__ void unit_pass_q(const FfnArgs& a, const Segment& seg, int t0, int r0,
+                                            int K, const uint8_t* C0, const uint8_t* C1,
+                                            const uint16_t* S0, const uint16_t* S1, f32x4* red) {
+  constexpr int NM = kMode == 0 ? 2 : 1;
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wave = threadIdx.x >> 6;
+  const int rA = lane & 15, gK = lane >> 4;
+  const int nss = K / 128;
+  const int lo = wave * nss / W, hi = (wave + 1) * nss / W;
+
+  // fp16 activations in expansion order: x16 for gate-up, Hh for down.
+  const uint16_t* X = static_cast<const uint16_t*>(kMode == 0 ? a.x16 : a.hh);
+  const int ldx = kMode == 0 ? a.H : a.ldh;
+  const u32x4* xb[T];
+#pragma unroll
+  for (int tt = 0; tt < T; ++tt) {
+    const int t = min(t0 + tt * 16 + rA, seg.n - 1);
+    xb[tt] = reinterpret_cast<const u32x4*>(X + (size_t)x_row(a, kMode, seg, t) * ldx) + 4 * gK;
+  }
+  const u32x4* pc[NM * R];
+  const uint16_t* ps[NM * R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const size_t row = (size_t)(r0 + 16 * r + rA);
+    pc[r] = reinterpret_cast<const u32x4*>(C0 + row * (K / 2)) + gK;
+    ps[r] = S0 + row * (K / 32) + gK;
+    if (NM > 1) {
+      pc[R + r] = reinterpret_cast<const u32x4*>(C1 + row * (K / 2)) + gK;
+      ps[R + r] = S1 + row * (K / 32) + gK;
+    }
+  }
+
+  f32x4 acc[NM][R][T];
+#pragma unroll
+  for (int m = 0; m < NM; ++m)
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+#pragma unroll
+      for (int tt = 0; tt < T; ++tt) acc[m][r][tt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  if (hi > lo) {
+    StageQ<T, R, NM> st0, st1;
+    load_q(st0, pc, ps, xb, lo, hi);
+    for (int s = lo; s < hi; s += 2) {
+      if (s + 1 < hi) load_q(st1, pc, ps, xb, s + 1, hi);
+      compute_q(st0, acc, s, hi);
+      if (s + 1 >= hi) break;
+      if (s + 2 < hi) load_q(st0, pc, ps, xb, s + 2, hi);
+      compute_q(st1, acc, s + 1, hi);
+    }
+  }
+
+  if (W > 1) {
+    constexpr int kTiles = NM * R * TMAX;
+#pragma unroll
+    for (int m = 0; m < NM; ++m)
+#pragma unroll
+      for (int r = 0; r < R; ++r)
+#pragma unroll
+        for (int tt = 0; tt < T; ++tt)
+          red[(wave * kTiles + (m * R + r) * TMAX + tt) * kWave + lane] = acc[m][r][tt];
+    __syncthreads();
+    if (wave == 0) {
+      for (int w = 1; w < W; ++w) {
+#pragma unroll
+        for (int m = 0; m < NM; ++m)
+#pragma unroll
+          for (int r = 0; r < R; ++r)
+#pragma unroll
+            for (int tt = 0; tt < T; ++tt) {
+              const f32x4 p = red[(w * kTiles + (m * R + r) * TMAX + tt) * kWave + lane];
+#pragma unroll
+              for (int i = 0; i < 4; ++i) acc[m][r][tt][i] += p[i];
+            }
+      }
+    }
+  }
+  if (wave == 0) {
+#pragma unroll
+    for (int tt = 0; tt < T; ++tt) {
+      const int t = t0 + tt * 16 + rA;
+      if (t >= seg.n) continue;
+      if (kMode == 0) {
+        _Float16* dst = static_cast<_Float16*>(a.hh) + (size_t)(seg.base + t) * a.ldh;
+#pragma unroll
+        for (int r = 0; r < R; ++r)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int f = r0 + 16 * r + 4 * gK + i;
+            dst[(f & ~7) + perm8(f & 7)] = (_Float16)(silu(acc[0][r][tt][i]) * acc[NM - 1][r][tt][i]);
+          }
+      } else {
+        float* dst = a.out + (size_t)out_row(a, seg, t) * a.H;
+#pragma unroll
+        for (int r = 0; r < R; ++r)
+          *reinterpret_cast<f32x4*>(dst + r0 + 16 * r + 4 * gK) = acc[0][r][tt];
+      }
+    }
+  }
+  if (W > 1) __syncthreads();
+}
+
+template <int kMode, int TMAX, int R, int W>
+__global__ __launch_bounds__(W * 64) void ffn_q4_kernel(FfnArgs a) {
+  constexpr int NM = kMode == 0 ? 2 : 1;
+  __shared__ f32x4 red[W > 1 ? W * NM * R * TMAX * kWave : 1];
+  Segment seg;
+  int unit;
+  if (!resolve_block(a, kMode, 16 * R, &seg, &unit)) return;
+  const int r0 = unit * 16 * R;
+  const int rows = kMode == 0 ? (seg.shared ? a.Fs : a.F) : a.H;
+  const int K = kMode == 0 ? a.H : (seg.shared ? a.Fs : a.F);
+  const size_t mat = (size_t)rows * K;
+  const void *M0, *M1, *Q0, *Q1;
+  if (kMode == 0) {
+    M0 = seg.shared ? a.sh_gate : a.gate;
+    M1 = seg.shared ? a.sh_up : a.up;
+    Q0 = seg.shared ? a.sh_gate_s : a.gate_s;
+    Q1 = seg.shared ? a.sh_up_s : a.up_s;
+  } else {
+    M0 = M1 = seg.shared ? a.sh_down : a.down;
+    Q0 = Q1 = seg.shared ? a.sh_down_s : a.down_s;
+  }
+  const uint8_t* C0 = static_cast<const uint8_t*>(M0) + seg.id * (mat / 2);
+  const uint8_t* C1 = static_cast<const uint8_t*>(M1) + seg.id * (mat / 2);
+  const uint16_t* S0 = static_cast<const uint16_t*>(Q0) + seg.id * (mat / 32);
+  const uint16_t* S1 = static_cast<const uint16_t*>(Q1) + seg.id * (mat / 32);
+  for (int t0 = 0; t0 < seg.n; t0 += 16 * TMAX) {
+    const int T = min(TMAX, (seg.n - t0 + 15) / 16);
+    if (TMAX >= 4 && T >= 4)
+      unit_pass_q<kMode, (TMAX >= 4 ? 4 : 1), TMAX, R, W>(a, seg, t0, r0, K, C0, C1, S0, S1, red);
+    else if (TMAX >= 3 && T == 3)
+      unit_pass_q<kMode, (TMAX >= 3 ? 3 : 1), TMAX, R, W>(a, seg, t0, r0, K, C0, C1, S0, S1, red);
+    else if (TMAX >= 2 && T == 2)
+      unit_pass_q<kMode, (TMAX >= 2 ? 2 : 1), TMAX, R, W>(a, seg, t0, r0, K, C0, C1, S0, S1, red);
+    else
+      unit_pass_q<kMode, 1, TMAX, R, W>(a, seg, t0, r0, K, C0, C1, S0, S1, red);
+  }
+}
+
+// x [B, H] bf16 -> x16 [B, H] fp16 in expansion order, one 8-block per thread.
+__global__ __launch_bounds__(256) void q4_prep_x_kernel(const uint16_t* __restrict__ x,
+                                                        uint16_t* __restrict__ x16, int n8) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n8) return;
+  const u32x4 v = reinterpret_cast<const u32x4*>(x)[i];
+  _Float16 h[8], o[8];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    h[2 * q] = (_Float16)bf16_to_f32(v[q] & 0xFFFFu);
+    h[2 * q + 1] = (_Float16)bf16_to_f32(v[q] >> 16);
+  }
+#pragma unroll
+  for (int e = 0; e < 8; ++e) o[perm8(e)] = h[e];
+  u32x4 r;
+  __builtin_memcpy(&r, o, 16);
+  reinterpret_cast<u32x4*>(x16)[i] = r;
+}
+
+#ifndef S2MOE_Q4_STEPS_PER_WAVE
+#define S2MOE_Q4_STEPS_PER_WAVE 8
+#endif
+
+int pick_waves_q4(int nss, int tiles) {
+  int w = 1;
+  while (w * 2 <= 8 && nss / (w * 2) >= S2MOE_Q4_STEPS_PER_WAVE && (w * 2) * tiles <= 32)
+    w *= 2;
+  return w;
+}
+
+template <int kMode, int TMAX, int R>
+hipError_t launch_q4_mode(const FfnArgs& a, hipStream_t s) {
+  const int nm = kMode == 0 ? 2 : 1;
+  int nss = kMode == 0 ? a.H / 128 : a.F / 128;
+  if (kMode == 1 && a.S > 0) nss = min(nss, a.Fs / 128);
+  const int w = pick_waves_q4(nss, nm * R * TMAX);
+  const dim3 grid(n_blocks(a, kMode, 16 * R));
+  switch (w) {
+    case 1: hipLaunchKernelGGL((ffn_q4_kernel<kMode, TMAX, R, 1>), grid, dim3(64), 0, s, a); break;
+    case 2: hipLaunchKernelGGL((ffn_q4_kernel<kMode, TMAX, R, 2>), grid, dim3(128), 0, s, a); break;
+    case 4: hipLaunchKernelGGL((ffn_q4_kernel<kMode, TMAX, R, 4>), grid, dim3(256), 0, s, a); break;
+    default: hipLaunchKernelGGL((ffn_q4_kernel<kMode, TMAX, R, 8>), grid, dim3(512), 0, s, a); break;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_ffn_q4(const FfnArgs& a, hipStream_t s) {
+  const int n8 = a.B * a.H / 8;
+  hipLaunchKernelGGL(q4_prep_x_kernel, dim3((n8 + 255) / 256), dim3(256), 0, s,
+                     static_cast<const uint16_t*>(a.x), static_cast<uint16_t*>(a.x16), n8);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return err;
+  if (a.B <= 16) {
+    err = launch_q4_mode<0, 1, 2>(a, s);
+    return err != hipSuccess ? err : launch_q4_mode<1, 1, 4>(a, s);
+  }
+  if (a.B <= 32) {
+    err = launch_q4_mode<0, 2, 1>(a, s);
+    return err != hipSuccess ? err : launch_q4_mode<1, 2, 2>(a, s);
+  }
+  err = launch_q4_mode<0, 4, 1>(a, s);
+  return err != hipSuccess ? err : launch_q4_mode<1, 4, 1>(a, s);
+}
+
+}  // namespace s2moe

@@ -59,8 +59,9 @@ struct FfnArgs {
   const void *gate_s, *up_s, *down_s;
   const void *sh_gate, *sh_up, *sh_down;
   const void *sh_gate_s, *sh_up_s, *sh_down_s;
-  void* hh;  // workspace: SwiGLU activations [B*k + S*B, ldh] (fp32 or bf16)
+  void* hh;  // workspace: SwiGLU activations [B*k + S*B, ldh] (fp32, bf16 or fp16)
   int ldh;
+  void* x16;  // workspace, int4 weights only: x as fp16 [B, H] in decode order
   float* out;  // [B*k + S*B, H]
 };
 
@@ -75,6 +76,7 @@ hipError_t launch_route(const RouteArgs& a, hipStream_t s);
 hipError_t launch_reuse_gate(const GateArgs& a, hipStream_t s);
 hipError_t launch_ffn(const FfnArgs& a, hipStream_t s);
 hipError_t launch_ffn_bf16(const FfnArgs& a, hipStream_t s);
+hipError_t launch_ffn_q4(const FfnArgs& a, hipStream_t s);
 hipError_t launch_combine(const CombineArgs& a, hipStream_t s);
 
 }  // namespace s2moe
