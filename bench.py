@@ -43,6 +43,45 @@ def expert_bytes(shape, F: int) -> int:
     return n // 2 + 2 * (n // 32)  # 4-bit codes + one fp16 scale per 32
 
 
+FFN_SOURCES = {
+    "bf16": ["ffn_bf16.hip", "ffn_common.h", "common.h", "kernels.h"],
+    "q4g32": ["ffn_q4.hip", "ffn_common.h", "common.h", "kernels.h"],
+    "f32": ["ffn.hip", "ffn_common.h", "common.h", "kernels.h"],
+}
+
+
+def ffn_source_hash(wdt: str) -> str:
+    """sha256 of the sources the expert-FFN kernels of this weight format are
+    built from (identifies the kernel a traffic measurement belongs to)."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in FFN_SOURCES[wdt]:
+        with open(os.path.join(ROOT, "paper_2608_15018_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def recorded_traffic(name: str, wdt: str):
+    """HBM bytes per s2moe_verify_moe call from the committed rocprofv3 counter
+    summary of this workload, or None if there is none or the kernel sources
+    changed since it was taken."""
+    path = os.path.join(ROOT, "profiles", f"verify_moe_{name}_traffic.md")
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    with open(path) as f:
+        for line in f:
+            k, _, v = line.strip().lstrip("- ").partition(":")
+            if k in ("traffic_bytes_per_launch", "kernel_source_sha256"):
+                vals[k] = v.strip().strip("`")
+    if vals.get("kernel_source_sha256") != ffn_source_hash(wdt):
+        return None
+    try:
+        return int(vals["traffic_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -53,6 +92,8 @@ def main(argv=None):
     ap.add_argument("--alpha", type=float, default=None)
     ap.add_argument("--seed", type=int, default=1)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="only run a plain device copy of 1 GiB (calibrates HBM byte counters)")
     args = ap.parse_args(argv)
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -66,8 +107,19 @@ def main(argv=None):
     from synth import gen
     from synth.configs import WORKLOAD_ID, WORKLOADS
 
-    s2.load()
     torch.cuda.set_device(0)
+    if args.copy_probe:
+        # A plain copy of known size: each launch reads and writes 1 GiB.
+        n = 1 << 30
+        src = torch.ones(n // 4, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_probe_bytes_read": n, "copy_probe_bytes_written": n,
+                          "launches": 5}))
+        return 0
+    s2.load()
     wl = WORKLOADS[args.workload]
     shape = wl.shape if args.alpha is None else wl.shape.with_(alpha=args.alpha)
     B = args.batch or wl.batches[-1 if args.workload == "c5" else 0]
@@ -155,7 +207,8 @@ def main(argv=None):
                    "top_k": shape.top_k, "shared": shape.n_shared, "cap": shape.cap,
                    "alpha": shape.alpha},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": recorded_traffic(wl.name, shape.wdt),
                      "kernel": "s2moe_verify_moe (expert gate-up + down launches)",
                      "bytes_per_launch": unique_bytes, "avg_launch_us": ffn_avg_s * 1e6},
         "cpu_baseline": cpu,
