@@ -92,6 +92,8 @@ def main(argv=None):
     ap.add_argument("--alpha", type=float, default=None)
     ap.add_argument("--seed", type=int, default=1)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--plain-weights", action="store_true",
+                    help="stream the row-major weights instead of the packed tile order")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run a plain device copy of 1 GiB (calibrates HBM byte counters)")
     args = ap.parse_args(argv)
@@ -132,10 +134,16 @@ def main(argv=None):
     shared = gen.make_shared_experts(shape, args.seed, 0, wid, wl.w_std)
     _log(f"[bench] inputs generated in {time.time() - t0:.1f}s")
 
-    layer = s2.make_layer(shape)
+    # Weights are packed once, as at model load (s2moe_pack_weights); the
+    # verify step then streams each activated expert's tiles contiguously.
+    packed = shape.wdt != "f32" and not args.plain_weights
+    layer = s2.make_layer(shape, flags=shape.flags | (s2.PACKED_WEIGHTS if packed else 0))
     p = s2.VerifyPass(layer, B)
     xd, rd, cd = s2.to_device(x), s2.to_device(router), s2.to_device(conf_w)
     dev_w, wstruct = s2.weights_to_device(experts, shared)
+    if packed:
+        dev_w, wstruct = s2.pack_expert_weights(dev_w, shape.wdt)
+        torch.cuda.synchronize()
     stream = torch.cuda.current_stream()
 
     # warm-up (also fixes the routing, which is deterministic)
@@ -205,7 +213,7 @@ def main(argv=None):
         "config": {"workload": wl.description, "name": wl.name, "draft_tokens": B,
                    "hidden": shape.hidden, "ffn": shape.ffn, "experts": shape.n_experts,
                    "top_k": shape.top_k, "shared": shape.n_shared, "cap": shape.cap,
-                   "alpha": shape.alpha},
+                   "alpha": shape.alpha, "weights": "packed" if packed else "row-major"},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
                      "traffic": recorded_traffic(wl.name, shape.wdt),

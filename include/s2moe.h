@@ -72,7 +72,10 @@ enum {
   /* lambda_b = alpha instead of alpha * gap_b. */
   S2MOE_BIAS_ABSOLUTE = 2u,
   /* gate weights from the biased logits ell' instead of the original ell. */
-  S2MOE_GATE_FROM_BIASED = 4u
+  S2MOE_GATE_FROM_BIASED = 4u,
+  /* The expert weights passed to s2moe_verify_moe were re-laid by
+     s2moe_pack_weights (BF16 and Q4G32 only). */
+  S2MOE_PACKED_WEIGHTS = 8u
 };
 
 /* One MoE layer.  Supported (act_dtype, w_dtype) pairs: (F32, F32),
@@ -154,6 +157,25 @@ s2moe_status s2moe_verify_moe(const s2moe_layer *layer, int32_t n_tokens, const 
                               const s2moe_weights *w, const s2moe_routing *r,
                               void *workspace, size_t workspace_bytes, float *expert_out,
                               void *stream);
+
+/* Re-lay n_mats expert matrices of [rows, cols] (K = cols contiguous) into
+   the tile order the matrix-core kernels stream (layer flag
+   S2MOE_PACKED_WEIGHTS).  A one-time transform at model load, not part of
+   a verify step: the values are unchanged, only their order, and dst has the
+   same size as src.
+     BF16:  src, dst [n_mats, rows, cols] bf16; each 16-row x 32-column tile
+            becomes one contiguous 1 KB block, tiles ordered row-tile-major.
+            rows % 16 == 0, cols % 32 == 0.  *_scales ignored (may be NULL).
+     Q4G32: src, dst codes [n_mats, rows, cols/2]; src_scales, dst_scales
+            fp16 [n_mats, rows, cols/32]; each 16-row x 128-column block of
+            codes becomes 1 KB, its 64 scales 128 bytes.  rows % 16 == 0,
+            cols % 128 == 0.
+   Apply it to gate and up as [E, F, H], down as [E, H, F], and the shared
+   matrices alike.  dst must not overlap src.  Device pointers, enqueued on
+   `stream`; F32 weights give S2MOE_EUNSUPPORTED. */
+s2moe_status s2moe_pack_weights(int32_t w_dtype, int32_t n_mats, int32_t rows, int32_t cols,
+                                const void *src, const void *src_scales, void *dst,
+                                void *dst_scales, void *stream);
 
 /* Combine: y_b = sum_{j<k} gate_w[b,j] expert_out[b*k+j] +
    sum_{s<S} expert_out[B*k + s*B + b], summed in that order (fp32). */

@@ -9,6 +9,7 @@ from ._lib import (  # noqa: F401
     BIAS_ABSOLUTE,
     F32,
     GATE_FROM_BIASED,
+    PACKED_WEIGHTS,
     PREF_ACTIVATED_ONLY,
     Q4G32,
     Layer,
@@ -20,9 +21,15 @@ from ._lib import (  # noqa: F401
     load,
     make_layer,
     make_weights,
+    pack_weights,
     reuse_gate,
     route,
     verify_moe,
     workspace_bytes,
 )
-from .pipeline import VerifyPass, to_device, weights_to_device  # noqa: F401
+from .pipeline import (  # noqa: F401
+    VerifyPass,
+    pack_expert_weights,
+    to_device,
+    weights_to_device,
+)

@@ -23,7 +23,7 @@ HEADER_PATH = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__fil
 
 F32, BF16, Q4G32 = 0, 1, 2
 DTYPE_CODES = {"f32": F32, "bf16": BF16, "q4g32": Q4G32}
-PREF_ACTIVATED_ONLY, BIAS_ABSOLUTE, GATE_FROM_BIASED = 1, 2, 4
+PREF_ACTIVATED_ONLY, BIAS_ABSOLUTE, GATE_FROM_BIASED, PACKED_WEIGHTS = 1, 2, 4, 8
 OK, EINVAL, EUNSUPPORTED, EWORKSPACE, EHIP = 0, 1, 2, 3, 4
 
 
@@ -79,6 +79,9 @@ def load():
     lib.s2moe_verify_moe.argtypes = [Lp, ctypes.c_int32, P, ctypes.POINTER(Weights),
                                      ctypes.POINTER(RoutingStruct), P, ctypes.c_size_t, P, P]
     lib.s2moe_combine.argtypes = [Lp, ctypes.c_int32, ctypes.POINTER(RoutingStruct), P, P, P]
+    lib.s2moe_pack_weights.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                                       ctypes.c_int32, P, P, P, P, P]
+    lib.s2moe_pack_weights.restype = ctypes.c_int
     for f in ("s2moe_route", "s2moe_reuse_gate", "s2moe_verify_moe", "s2moe_combine"):
         getattr(lib, f).restype = ctypes.c_int
     lib.s2moe_last_error.restype = ctypes.c_char_p
@@ -223,6 +226,20 @@ def verify_moe(layer: Layer, x: torch.Tensor, weights: Weights, rt: Routing,
 def combine(layer: Layer, rt: Routing, expert_out: torch.Tensor, y: torch.Tensor, stream=None):
     _check(load().s2moe_combine(ctypes.byref(layer), rt.B, ctypes.byref(rt.struct),
                                 _ptr(expert_out), _ptr(y), _stream(stream)))
+
+
+def pack_weights(wdt: str, mats: torch.Tensor, scales: torch.Tensor | None = None,
+                 stream=None):
+    """Packed copies (s2moe_pack_weights) of matrices [n, rows, cols] (bf16) or
+    of int4 codes [n, rows, cols/2] with their scales [n, rows, cols/32]."""
+    code = DTYPE_CODES[wdt]
+    n, rows = mats.shape[0], mats.shape[1]
+    cols = mats.shape[2] * (2 if code == Q4G32 else 1)
+    dst = torch.empty_like(mats)
+    dst_s = torch.empty_like(scales) if scales is not None else None
+    _check(load().s2moe_pack_weights(code, n, rows, cols, _ptr(mats), _ptr(scales), _ptr(dst),
+                                     _ptr(dst_s), _stream(stream)))
+    return dst, dst_s
 
 
 def abi_version() -> int:

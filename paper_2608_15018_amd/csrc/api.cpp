@@ -64,7 +64,7 @@ s2moe_status check_layer(const char* fn, const s2moe_layer* L, int32_t B) {
                 L->top_k, L->n_experts);
   if (!std::isfinite(L->alpha) || L->alpha < 0.f)
     return fail(S2MOE_EINVAL, "%s: alpha = %g must be finite and >= 0", fn, (double)L->alpha);
-  if (L->flags & ~7u) return fail(S2MOE_EINVAL, "%s: unknown flags 0x%x", fn, L->flags);
+  if (L->flags & ~15u) return fail(S2MOE_EINVAL, "%s: unknown flags 0x%x", fn, L->flags);
   if (L->n_shared < 0) return fail(S2MOE_EINVAL, "%s: n_shared = %d < 0", fn, L->n_shared);
   if (L->n_shared > S2MOE_MAX_SHARED)
     return fail(S2MOE_EUNSUPPORTED, "%s: n_shared = %d exceeds %d", fn, L->n_shared,
@@ -89,6 +89,8 @@ s2moe_status check_layer(const char* fn, const s2moe_layer* L, int32_t B) {
       (L->hidden % 256 || L->ffn % 256 || (L->n_shared > 0 && L->ffn_shared % 256)))
     return fail(S2MOE_EUNSUPPORTED,
                 "%s: Q4G32 weights need hidden, ffn and ffn_shared multiples of 256", fn);
+  if ((L->flags & S2MOE_PACKED_WEIGHTS) && wdt == S2MOE_F32)
+    return fail(S2MOE_EUNSUPPORTED, "%s: S2MOE_PACKED_WEIGHTS needs BF16 or Q4G32 weights", fn);
   return S2MOE_OK;
 }
 
@@ -281,7 +283,50 @@ s2moe_status s2moe_verify_moe(const s2moe_layer* layer, int32_t n_tokens, const 
   a.ldh = (layer->n_shared > 0 && layer->ffn_shared > layer->ffn) ? layer->ffn_shared
                                                                    : layer->ffn;
   a.out = expert_out;
+  a.packed = (layer->flags & S2MOE_PACKED_WEIGHTS) != 0;
   return hip_status(fn, s2moe::launch_ffn(a, static_cast<hipStream_t>(stream)));
+}
+
+s2moe_status s2moe_pack_weights(int32_t w_dtype, int32_t n_mats, int32_t rows, int32_t cols,
+                                const void* src, const void* src_scales, void* dst,
+                                void* dst_scales, void* stream) {
+  const char* fn = "s2moe_pack_weights";
+  if (w_dtype != S2MOE_BF16 && w_dtype != S2MOE_Q4G32)
+    return fail(w_dtype == S2MOE_F32 ? S2MOE_EUNSUPPORTED : S2MOE_EINVAL,
+                "%s: w_dtype = %d; packing applies to BF16 and Q4G32 weights", fn, w_dtype);
+  const bool q4 = w_dtype == S2MOE_Q4G32;
+  if (n_mats < 1 || rows < 16 || rows % 16 != 0)
+    return fail(S2MOE_EINVAL, "%s: n_mats = %d, rows = %d (need n_mats >= 1, rows % 16 == 0)",
+                fn, n_mats, rows);
+  const int kq = q4 ? 128 : 32;
+  if (cols < kq || cols % kq != 0)
+    return fail(S2MOE_EINVAL, "%s: cols = %d must be a positive multiple of %d", fn, cols, kq);
+  S2MOE_REQUIRE_PTR(src);
+  S2MOE_REQUIRE_PTR(dst);
+  const size_t bytes = (size_t)n_mats * rows * cols / (q4 ? 2 : 1) * (q4 ? 1 : 2);
+  const char* s0 = static_cast<const char*>(src);
+  const char* d0 = static_cast<const char*>(dst);
+  if (s0 < d0 + bytes && d0 < s0 + bytes)
+    return fail(S2MOE_EINVAL, "%s: src and dst overlap (packing is not in place)", fn);
+  if (q4) {
+    S2MOE_REQUIRE_PTR(src_scales);
+    S2MOE_REQUIRE_PTR(dst_scales);
+    const size_t sb = (size_t)n_mats * rows * (cols / 32) * 2;
+    const char* ss = static_cast<const char*>(src_scales);
+    const char* ds = static_cast<const char*>(dst_scales);
+    if (ss < ds + sb && ds < ss + sb)
+      return fail(S2MOE_EINVAL, "%s: src_scales and dst_scales overlap", fn);
+  }
+  s2moe::PackArgs a;
+  a.src = src;
+  a.src_s = src_scales;
+  a.dst = dst;
+  a.dst_s = dst_scales;
+  a.n = n_mats;
+  a.rows = rows;
+  a.K = cols;
+  a.q4 = q4;
+  return hip_status(fn, s2moe::launch_pack(a, static_cast<hipStream_t>(stream)));
 }
 
 s2moe_status s2moe_combine(const s2moe_layer* layer, int32_t n_tokens, const s2moe_routing* r,

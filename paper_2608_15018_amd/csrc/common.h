@@ -114,26 +114,40 @@ __device__ __forceinline__ float wave_max_dpp(float v) {
   return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
 }
 
-// 48-bit ranking key of expert e with value v: value descending first, then
-// expert id ascending.  0 marks an empty slot (below every real key).
-__device__ __forceinline__ uint64_t rank_key(float v, int e) {
-  return ((uint64_t)order_key(v) << 16) | (uint32_t)(0xFFFF - e);
-}
-
-// The k-th largest of the distinct keys held four per lane (bit-by-bit
-// search of the threshold: ballots count the keys at or above a candidate).
-// Exactly k keys are >= the result.  Wave-uniform.
-__device__ __forceinline__ uint64_t wave_kth_key(const uint64_t key[4], int nj, int k) {
-  uint64_t prefix = 0;
-  for (int bit = 47; bit >= 0; --bit) {
-    const uint64_t cand = prefix | (1ull << bit);
-    int cnt = 0;
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-      if (j < nj) cnt += __popcll(__ballot(key[j] >= cand));
-    if (cnt >= k) prefix = cand;
+// Value of the k-th largest entry (duplicates counted) among the order keys
+// held four per lane: a bit-by-bit search of the largest threshold with at
+// least k keys at or above it (ballots count them).  Empty slots hold 0,
+// below every real key.  Wave-uniform, branch-free apart from the loop.
+__device__ __forceinline__ uint32_t wave_kth_key(const uint32_t key[4], int k) {
+  uint32_t prefix = 0;
+#pragma unroll 4
+  for (int bit = 31; bit >= 0; --bit) {
+    const uint32_t cand = prefix | (1u << bit);
+    const int cnt = __popcll(__ballot(key[0] >= cand)) + __popcll(__ballot(key[1] >= cand)) +
+                    __popcll(__ballot(key[2] >= cand)) + __popcll(__ballot(key[3] >= cand));
+    prefix = cnt >= k ? cand : prefix;
   }
   return prefix;
+}
+
+// Flags (bit j of a lane) of the k best entries under (value desc, expert id
+// asc), given kth = wave_kth_key(key, k): every key above kth, plus the keys
+// equal to kth with the smallest expert ids (expert lane + 64 j) up to k.
+__device__ __forceinline__ uint32_t wave_select_top(const uint32_t key[4], uint32_t kth, int k) {
+  const int above = __popcll(__ballot(key[0] > kth)) + __popcll(__ballot(key[1] > kth)) +
+                    __popcll(__ballot(key[2] > kth)) + __popcll(__ballot(key[3] > kth));
+  const int need = k - above;
+  const uint64_t lt = lanemask_lt();
+  uint32_t bits = 0;
+  int before = 0;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const uint64_t m = __ballot(key[j] == kth);
+    const int r = before + __popcll(m & lt);
+    if (key[j] > kth || (key[j] == kth && r < need)) bits |= 1u << j;
+    before += __popcll(m);
+  }
+  return bits;
 }
 
 // Rank, in ascending expert id, of the flagged experts: expert lane + 64 j

@@ -26,7 +26,16 @@ struct Stage {
   u32x4 b[T][U];
 };
 
-template <int T, int R, int NM, int U>
+// Weights of step s: plain layout -> 16 bytes at u32x4 index 4 s of the
+// lane's row pointer; packed layout -> 1 KB tile s (u32x4 index 64 s), read
+// with a nontemporal hint since each weight byte is used once per call.
+template <bool kPacked>
+__device__ __forceinline__ u32x4 load_weights(const u32x4* p, int s) {
+  if (kPacked) return __builtin_nontemporal_load(p + 64 * s);
+  return p[4 * s];
+}
+
+template <bool kPacked, int T, int R, int NM, int U>
 __device__ __forceinline__ void load_stage(Stage<T, R, NM, U>& st, const u32x4* const* pa,
                                            const u32x4* const* xb, int s0, int hi) {
 #pragma unroll
@@ -35,7 +44,7 @@ __device__ __forceinline__ void load_stage(Stage<T, R, NM, U>& st, const u32x4* 
 #pragma unroll
     for (int m = 0; m < NM; ++m)
 #pragma unroll
-      for (int r = 0; r < R; ++r) st.a[m][r][u] = pa[m * R + r][4 * s];
+      for (int r = 0; r < R; ++r) st.a[m][r][u] = load_weights<kPacked>(pa[m * R + r], s);
   }
 #pragma unroll
   for (int tt = 0; tt < T; ++tt)
@@ -62,7 +71,7 @@ __device__ __forceinline__ void compute_stage(const Stage<T, R, NM, U>& st,
 }
 
 // One pass over up to 16*T tokens of the unit, all of the wave's K range.
-template <int kMode, int T, int TMAX, int R, int W, int U>
+template <int kMode, int T, int TMAX, int R, int W, int U, bool kPacked>
 __device__ __forceinline__ void unit_pass(const FfnArgs& a, const Segment& seg, int t0, int r0,
                                           int K, const uint16_t* W0, const uint16_t* W1,
                                           f32x4* red) {
@@ -84,9 +93,15 @@ __device__ __forceinline__ void unit_pass(const FfnArgs& a, const Segment& seg, 
   const u32x4* pa[NM * R];
 #pragma unroll
   for (int r = 0; r < R; ++r) {
-    pa[r] = reinterpret_cast<const u32x4*>(W0 + (size_t)(r0 + 16 * r + rA) * K) + gK;
-    if (NM > 1)
-      pa[R + r] = reinterpret_cast<const u32x4*>(W1 + (size_t)(r0 + 16 * r + rA) * K) + gK;
+    if (kPacked) {
+      const size_t tile0 = (size_t)(r0 / 16 + r) * nks;  // first tile of the row tile
+      pa[r] = reinterpret_cast<const u32x4*>(W0) + tile0 * 64 + lane;
+      if (NM > 1) pa[R + r] = reinterpret_cast<const u32x4*>(W1) + tile0 * 64 + lane;
+    } else {
+      pa[r] = reinterpret_cast<const u32x4*>(W0 + (size_t)(r0 + 16 * r + rA) * K) + gK;
+      if (NM > 1)
+        pa[R + r] = reinterpret_cast<const u32x4*>(W1 + (size_t)(r0 + 16 * r + rA) * K) + gK;
+    }
   }
 
   f32x4 acc[NM][R][T];
@@ -99,12 +114,12 @@ __device__ __forceinline__ void unit_pass(const FfnArgs& a, const Segment& seg, 
   if (hi > lo) {
     const int nch = (hi - lo + U - 1) / U;
     Stage<T, R, NM, U> st0, st1;
-    load_stage(st0, pa, xb, lo, hi);
+    load_stage<kPacked>(st0, pa, xb, lo, hi);
     for (int c = 0; c < nch; c += 2) {
-      if (c + 1 < nch) load_stage(st1, pa, xb, lo + (c + 1) * U, hi);
+      if (c + 1 < nch) load_stage<kPacked>(st1, pa, xb, lo + (c + 1) * U, hi);
       compute_stage(st0, acc, lo + c * U, hi);
       if (c + 1 >= nch) break;
-      if (c + 2 < nch) load_stage(st0, pa, xb, lo + (c + 2) * U, hi);
+      if (c + 2 < nch) load_stage<kPacked>(st0, pa, xb, lo + (c + 2) * U, hi);
       compute_stage(st1, acc, lo + (c + 1) * U, hi);
     }
   }
@@ -165,7 +180,7 @@ __device__ __forceinline__ void unit_pass(const FfnArgs& a, const Segment& seg, 
   if (W > 1) __syncthreads();  // LDS is reused by the next pass
 }
 
-template <int kMode, int TMAX, int R, int W, int U>
+template <int kMode, int TMAX, int R, int W, int U, bool kPacked>
 __global__ __launch_bounds__(W * 64) void ffn_bf16_kernel(FfnArgs a) {
   constexpr int NM = kMode == 0 ? 2 : 1;
   __shared__ f32x4 red[W > 1 ? W * NM * R * TMAX * kWave : 1];
@@ -188,13 +203,13 @@ __global__ __launch_bounds__(W * 64) void ffn_bf16_kernel(FfnArgs a) {
   for (int t0 = 0; t0 < seg.n; t0 += 16 * TMAX) {
     const int T = min(TMAX, (seg.n - t0 + 15) / 16);
     if (TMAX >= 4 && T >= 4)
-      unit_pass<kMode, (TMAX >= 4 ? 4 : 1), TMAX, R, W, U>(a, seg, t0, r0, K, W0, W1, red);
+      unit_pass<kMode, (TMAX >= 4 ? 4 : 1), TMAX, R, W, U, kPacked>(a, seg, t0, r0, K, W0, W1, red);
     else if (TMAX >= 3 && T == 3)
-      unit_pass<kMode, (TMAX >= 3 ? 3 : 1), TMAX, R, W, U>(a, seg, t0, r0, K, W0, W1, red);
+      unit_pass<kMode, (TMAX >= 3 ? 3 : 1), TMAX, R, W, U, kPacked>(a, seg, t0, r0, K, W0, W1, red);
     else if (TMAX >= 2 && T == 2)
-      unit_pass<kMode, (TMAX >= 2 ? 2 : 1), TMAX, R, W, U>(a, seg, t0, r0, K, W0, W1, red);
+      unit_pass<kMode, (TMAX >= 2 ? 2 : 1), TMAX, R, W, U, kPacked>(a, seg, t0, r0, K, W0, W1, red);
     else
-      unit_pass<kMode, 1, TMAX, R, W, U>(a, seg, t0, r0, K, W0, W1, red);
+      unit_pass<kMode, 1, TMAX, R, W, U, kPacked>(a, seg, t0, r0, K, W0, W1, red);
   }
 }
 
@@ -215,20 +230,26 @@ int pick_waves(int nks, int tiles) {
   return w;
 }
 
-template <int kMode, int TMAX, int R, int U>
-hipError_t launch_mode(const FfnArgs& a, hipStream_t s) {
+template <int kMode, int TMAX, int R, int U, bool kPacked>
+hipError_t launch_mode_p(const FfnArgs& a, hipStream_t s) {
   const int nm = kMode == 0 ? 2 : 1;
   int nks = kMode == 0 ? a.H / 32 : a.F / 32;
   if (kMode == 1 && a.S > 0) nks = min(nks, a.Fs / 32);
   const int w = pick_waves(nks, nm * R * TMAX);
   const dim3 grid(n_blocks(a, kMode, 16 * R));
   switch (w) {
-    case 1: hipLaunchKernelGGL((ffn_bf16_kernel<kMode, TMAX, R, 1, U>), grid, dim3(64), 0, s, a); break;
-    case 2: hipLaunchKernelGGL((ffn_bf16_kernel<kMode, TMAX, R, 2, U>), grid, dim3(128), 0, s, a); break;
-    case 4: hipLaunchKernelGGL((ffn_bf16_kernel<kMode, TMAX, R, 4, U>), grid, dim3(256), 0, s, a); break;
-    default: hipLaunchKernelGGL((ffn_bf16_kernel<kMode, TMAX, R, 8, U>), grid, dim3(512), 0, s, a); break;
+    case 1: hipLaunchKernelGGL((ffn_bf16_kernel<kMode, TMAX, R, 1, U, kPacked>), grid, dim3(64), 0, s, a); break;
+    case 2: hipLaunchKernelGGL((ffn_bf16_kernel<kMode, TMAX, R, 2, U, kPacked>), grid, dim3(128), 0, s, a); break;
+    case 4: hipLaunchKernelGGL((ffn_bf16_kernel<kMode, TMAX, R, 4, U, kPacked>), grid, dim3(256), 0, s, a); break;
+    default: hipLaunchKernelGGL((ffn_bf16_kernel<kMode, TMAX, R, 8, U, kPacked>), grid, dim3(512), 0, s, a); break;
   }
   return hipGetLastError();
+}
+
+template <int kMode, int TMAX, int R, int U>
+hipError_t launch_mode(const FfnArgs& a, hipStream_t s) {
+  return a.packed ? launch_mode_p<kMode, TMAX, R, U, true>(a, s)
+                  : launch_mode_p<kMode, TMAX, R, U, false>(a, s);
 }
 
 }  // namespace

@@ -70,7 +70,10 @@ struct StageQ {
   u32x4 b[T][4];      // 4 x 8 activations per token tile
 };
 
-template <int T, int R, int NM>
+// Codes and scale of super-step s: plain layout -> u32x4 index 4 s and
+// scale index 4 s of the lane's row pointers; packed layout -> 1 KB code
+// tile s and 128-byte scale tile s (nontemporal: read once per call).
+template <bool kPacked, int T, int R, int NM>
 __device__ __forceinline__ void load_q(StageQ<T, R, NM>& st, const u32x4* const* pc,
                                        const uint16_t* const* ps, const u32x4* const* xb,
                                        int s, int hi) {
@@ -79,8 +82,13 @@ __device__ __forceinline__ void load_q(StageQ<T, R, NM>& st, const u32x4* const*
   for (int m = 0; m < NM; ++m)
 #pragma unroll
     for (int r = 0; r < R; ++r) {
-      st.c[m][r] = pc[m * R + r][4 * s];
-      st.s[m][r] = ps[m * R + r][4 * s];
+      if (kPacked) {
+        st.c[m][r] = __builtin_nontemporal_load(pc[m * R + r] + 64 * s);
+        st.s[m][r] = __builtin_nontemporal_load(ps[m * R + r] + 64 * s);
+      } else {
+        st.c[m][r] = pc[m * R + r][4 * s];
+        st.s[m][r] = ps[m * R + r][4 * s];
+      }
     }
 #pragma unroll
   for (int tt = 0; tt < T; ++tt)
@@ -110,7 +118,7 @@ __device__ __forceinline__ void compute_q(const StageQ<T, R, NM>& st, f32x4 (&ac
     }
 }
 
-template <int kMode, int T, int TMAX, int R, int W>
+template <int kMode, int T, int TMAX, int R, int W, bool kPacked>
 __device__ __forceinline__ void unit_pass_q(const FfnArgs& a, const Segment& seg, int t0, int r0,
                                             int K, const uint8_t* C0, const uint8_t* C1,
                                             const uint16_t* S0, const uint16_t* S1, f32x4* red) {
@@ -134,12 +142,22 @@ __device__ __forceinline__ void unit_pass_q(const FfnArgs& a, const Segment& seg
   const uint16_t* ps[NM * R];
 #pragma unroll
   for (int r = 0; r < R; ++r) {
-    const size_t row = (size_t)(r0 + 16 * r + rA);
-    pc[r] = reinterpret_cast<const u32x4*>(C0 + row * (K / 2)) + gK;
-    ps[r] = S0 + row * (K / 32) + gK;
-    if (NM > 1) {
-      pc[R + r] = reinterpret_cast<const u32x4*>(C1 + row * (K / 2)) + gK;
-      ps[R + r] = S1 + row * (K / 32) + gK;
+    if (kPacked) {
+      const size_t tile0 = (size_t)(r0 / 16 + r) * nss;  // first tile of the row tile
+      pc[r] = reinterpret_cast<const u32x4*>(C0) + tile0 * 64 + lane;
+      ps[r] = S0 + tile0 * 64 + lane;
+      if (NM > 1) {
+        pc[R + r] = reinterpret_cast<const u32x4*>(C1) + tile0 * 64 + lane;
+        ps[R + r] = S1 + tile0 * 64 + lane;
+      }
+    } else {
+      const size_t row = (size_t)(r0 + 16 * r + rA);
+      pc[r] = reinterpret_cast<const u32x4*>(C0 + row * (K / 2)) + gK;
+      ps[r] = S0 + row * (K / 32) + gK;
+      if (NM > 1) {
+        pc[R + r] = reinterpret_cast<const u32x4*>(C1 + row * (K / 2)) + gK;
+        ps[R + r] = S1 + row * (K / 32) + gK;
+      }
     }
   }
 
@@ -152,12 +170,12 @@ __device__ __forceinline__ void unit_pass_q(const FfnArgs& a, const Segment& seg
       for (int tt = 0; tt < T; ++tt) acc[m][r][tt] = f32x4{0.f, 0.f, 0.f, 0.f};
   if (hi > lo) {
     StageQ<T, R, NM> st0, st1;
-    load_q(st0, pc, ps, xb, lo, hi);
+    load_q<kPacked>(st0, pc, ps, xb, lo, hi);
     for (int s = lo; s < hi; s += 2) {
-      if (s + 1 < hi) load_q(st1, pc, ps, xb, s + 1, hi);
+      if (s + 1 < hi) load_q<kPacked>(st1, pc, ps, xb, s + 1, hi);
       compute_q(st0, acc, s, hi);
       if (s + 1 >= hi) break;
-      if (s + 2 < hi) load_q(st0, pc, ps, xb, s + 2, hi);
+      if (s + 2 < hi) load_q<kPacked>(st0, pc, ps, xb, s + 2, hi);
       compute_q(st1, acc, s + 1, hi);
     }
   }
@@ -212,7 +230,7 @@ __device__ __forceinline__ void unit_pass_q(const FfnArgs& a, const Segment& seg
   if (W > 1) __syncthreads();
 }
 
-template <int kMode, int TMAX, int R, int W>
+template <int kMode, int TMAX, int R, int W, bool kPacked>
 __global__ __launch_bounds__(W * 64) void ffn_q4_kernel(FfnArgs a) {
   constexpr int NM = kMode == 0 ? 2 : 1;
   __shared__ f32x4 red[W > 1 ? W * NM * R * TMAX * kWave : 1];
@@ -240,13 +258,13 @@ __global__ __launch_bounds__(W * 64) void ffn_q4_kernel(FfnArgs a) {
   for (int t0 = 0; t0 < seg.n; t0 += 16 * TMAX) {
     const int T = min(TMAX, (seg.n - t0 + 15) / 16);
     if (TMAX >= 4 && T >= 4)
-      unit_pass_q<kMode, (TMAX >= 4 ? 4 : 1), TMAX, R, W>(a, seg, t0, r0, K, C0, C1, S0, S1, red);
+      unit_pass_q<kMode, (TMAX >= 4 ? 4 : 1), TMAX, R, W, kPacked>(a, seg, t0, r0, K, C0, C1, S0, S1, red);
     else if (TMAX >= 3 && T == 3)
-      unit_pass_q<kMode, (TMAX >= 3 ? 3 : 1), TMAX, R, W>(a, seg, t0, r0, K, C0, C1, S0, S1, red);
+      unit_pass_q<kMode, (TMAX >= 3 ? 3 : 1), TMAX, R, W, kPacked>(a, seg, t0, r0, K, C0, C1, S0, S1, red);
     else if (TMAX >= 2 && T == 2)
-      unit_pass_q<kMode, (TMAX >= 2 ? 2 : 1), TMAX, R, W>(a, seg, t0, r0, K, C0, C1, S0, S1, red);
+      unit_pass_q<kMode, (TMAX >= 2 ? 2 : 1), TMAX, R, W, kPacked>(a, seg, t0, r0, K, C0, C1, S0, S1, red);
     else
-      unit_pass_q<kMode, 1, TMAX, R, W>(a, seg, t0, r0, K, C0, C1, S0, S1, red);
+      unit_pass_q<kMode, 1, TMAX, R, W, kPacked>(a, seg, t0, r0, K, C0, C1, S0, S1, red);
   }
 }
 
@@ -280,20 +298,26 @@ int pick_waves_q4(int nss, int tiles) {
   return w;
 }
 
-template <int kMode, int TMAX, int R>
-hipError_t launch_q4_mode(const FfnArgs& a, hipStream_t s) {
+template <int kMode, int TMAX, int R, bool kPacked>
+hipError_t launch_q4_mode_p(const FfnArgs& a, hipStream_t s) {
   const int nm = kMode == 0 ? 2 : 1;
   int nss = kMode == 0 ? a.H / 128 : a.F / 128;
   if (kMode == 1 && a.S > 0) nss = min(nss, a.Fs / 128);
   const int w = pick_waves_q4(nss, nm * R * TMAX);
   const dim3 grid(n_blocks(a, kMode, 16 * R));
   switch (w) {
-    case 1: hipLaunchKernelGGL((ffn_q4_kernel<kMode, TMAX, R, 1>), grid, dim3(64), 0, s, a); break;
-    case 2: hipLaunchKernelGGL((ffn_q4_kernel<kMode, TMAX, R, 2>), grid, dim3(128), 0, s, a); break;
-    case 4: hipLaunchKernelGGL((ffn_q4_kernel<kMode, TMAX, R, 4>), grid, dim3(256), 0, s, a); break;
-    default: hipLaunchKernelGGL((ffn_q4_kernel<kMode, TMAX, R, 8>), grid, dim3(512), 0, s, a); break;
+    case 1: hipLaunchKernelGGL((ffn_q4_kernel<kMode, TMAX, R, 1, kPacked>), grid, dim3(64), 0, s, a); break;
+    case 2: hipLaunchKernelGGL((ffn_q4_kernel<kMode, TMAX, R, 2, kPacked>), grid, dim3(128), 0, s, a); break;
+    case 4: hipLaunchKernelGGL((ffn_q4_kernel<kMode, TMAX, R, 4, kPacked>), grid, dim3(256), 0, s, a); break;
+    default: hipLaunchKernelGGL((ffn_q4_kernel<kMode, TMAX, R, 8, kPacked>), grid, dim3(512), 0, s, a); break;
   }
   return hipGetLastError();
+}
+
+template <int kMode, int TMAX, int R>
+hipError_t launch_q4_mode(const FfnArgs& a, hipStream_t s) {
+  return a.packed ? launch_q4_mode_p<kMode, TMAX, R, true>(a, s)
+                  : launch_q4_mode_p<kMode, TMAX, R, false>(a, s);
 }
 
 }  // namespace

@@ -7,8 +7,9 @@
 // small.  Nothing here is a serial loop over assignments:
 //   * g: one thread per expert sums w_b * ell_{b,e} over b in order;
 //   * TopCap: each expert's rank among the candidates by (g desc, id asc);
-//   * per token (one wave): biased keys, a bitwise threshold search for the
-//     k-th largest key, ballot ranks for ascending-id order, DPP softmax;
+//   * per token (one wave): biased order keys, a bitwise threshold search
+//     for the k-th largest value (ties to the lower expert id), ballot ranks
+//     for ascending-id order, DPP softmax;
 //   * buckets: a B-bit token mask per expert (LDS 64-bit ORs), so an
 //     assignment's position in its expert's list is the popcount of the mask
 //     below its token.
@@ -19,12 +20,15 @@
 
 namespace s2moe {
 
+constexpr int kStage = 10240;  // logits staged in LDS up to B * E = 10240
+
+template <bool kStaged>
 __global__ __launch_bounds__(1024) void reuse_gate_kernel(GateArgs a) {
   constexpr int kMaskWords = kMaxTokens / 64;
-  constexpr int kStage = 10240;  // logits staged in LDS up to B * E = 10240
-  __shared__ float ell_s[kStage];
+  __shared__ float ell_s[kStaged ? kStage : 1];
   __shared__ float w_s[kMaxTokens];
-  __shared__ float gm_s[kMaxExperts];  // g of candidates, -inf otherwise
+  __shared__ float gap_s[kMaxTokens];
+  __shared__ __align__(16) float gm_s[kMaxExperts];  // g of candidates, -inf otherwise
   __shared__ int pref_s[kMaxExperts];
   __shared__ int count_s[kMaxExperts];
   __shared__ int offset_s[kMaxExperts + 1];
@@ -37,22 +41,35 @@ __global__ __launch_bounds__(1024) void reuse_gate_kernel(GateArgs a) {
   const int wave = tid >> 6;
   const int n_waves = blockDim.x >> 6;
   const int B = a.B, E = a.E, k = a.k;
-  const bool staged = B * E <= kStage;
 
   // Non-negative confidences w_b; logits to LDS; cleared masks.
   int positive = 0;
   if (tid < B) {
     const float w = fmaxf(a.conf_w[tid], 0.f);
     w_s[tid] = w;
+    gap_s[tid] = a.gap[tid];
     positive = w > 0.f;
   }
-  if (staged)
-    for (int i = tid; i < B * E; i += blockDim.x) ell_s[i] = a.logits[i];
+  if (kStaged) {
+    // All loads first, then the LDS writes (10 per thread at most).
+    constexpr int kPer = kStage / 1024;
+    float v[kPer];
+#pragma unroll
+    for (int q = 0; q < kPer; ++q) {
+      const int i = tid + q * 1024;
+      v[q] = i < B * E ? a.logits[i] : 0.f;
+    }
+#pragma unroll
+    for (int q = 0; q < kPer; ++q) {
+      const int i = tid + q * 1024;
+      if (i < B * E) ell_s[i] = v[q];
+    }
+  }
   for (int i = tid; i < kMaxExperts * kMaskWords; i += blockDim.x)
     (&mask_s[0][0])[i] = 0ull;
   if (tid < kMaxExperts) cand_s[tid] = (!(a.flags & kPrefActivatedOnly) && tid < E) ? 1 : 0;
   const int active = __syncthreads_or(positive);
-  const float* ell = staged ? ell_s : a.logits;
+  const float* ell = kStaged ? static_cast<const float*>(ell_s) : a.logits;
 
   // TopCap candidates: all experts, or those in some token's plain top-k.
   if (a.flags & kPrefActivatedOnly) {
@@ -79,10 +96,14 @@ __global__ __launch_bounds__(1024) void reuse_gate_kernel(GateArgs a) {
     if (active && cand_s[tid]) {
       const float ge = gm_s[tid];
       int rank = 0;
-#pragma unroll 8
-      for (int e2 = 0; e2 < E; ++e2) {
-        const float g2 = gm_s[e2];
-        rank += (g2 > ge) || (g2 == ge && e2 < tid);
+      const f32x4* g4 = reinterpret_cast<const f32x4*>(gm_s);
+      for (int q = 0; q < (E + 3) / 4; ++q) {
+        const f32x4 g2 = g4[q];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int e2 = 4 * q + i;
+          rank += (e2 < E) && ((g2[i] > ge) || (g2[i] == ge && e2 < tid));
+        }
       }
       p = rank < a.cap;
     }
@@ -92,13 +113,12 @@ __global__ __launch_bounds__(1024) void reuse_gate_kernel(GateArgs a) {
   __syncthreads();
 
   // Per token: lambda_b, biased keys, biased top-k, gate weights, masks.
-  const int nj = (E + kWave - 1) / kWave;
   const bool from_biased = (a.flags & kGateFromBiased) != 0;
   for (int b = wave; b < B; b += n_waves) {
     float lam = 0.f;
-    if (active) lam = (a.flags & kBiasAbsolute) ? a.alpha : a.alpha * a.gap[b];
+    if (active) lam = (a.flags & kBiasAbsolute) ? a.alpha : a.alpha * gap_s[b];
     float l[4], lb[4];
-    uint64_t key[4];
+    uint32_t key[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int e = lane + kWave * j;
@@ -108,19 +128,14 @@ __global__ __launch_bounds__(1024) void reuse_gate_kernel(GateArgs a) {
       if (e < E) {
         l[j] = ell[(size_t)b * E + e];
         lb[j] = pref_s[e] ? l[j] + lam : l[j];
-        key[j] = rank_key(lb[j], e);
+        key[j] = order_key(lb[j]);
       }
     }
-    const uint64_t kth = wave_kth_key(key, nj, k);
-    uint32_t bits = 0;
+    const uint32_t bits = wave_select_top(key, wave_kth_key(key, k), k);
     float m = -INFINITY;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      if (key[j] != 0 && key[j] >= kth) {
-        bits |= 1u << j;
-        m = fmaxf(m, from_biased ? lb[j] : l[j]);
-      }
-    }
+    for (int j = 0; j < 4; ++j)
+      if ((bits >> j) & 1u) m = fmaxf(m, from_biased ? lb[j] : l[j]);
     int rank[4];
     wave_rank_flagged(bits, rank);
     m = wave_max_dpp(m);
@@ -206,7 +221,10 @@ __global__ __launch_bounds__(1024) void reuse_gate_kernel(GateArgs a) {
 }
 
 hipError_t launch_reuse_gate(const GateArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(reuse_gate_kernel, dim3(1), dim3(1024), 0, s, a);
+  if (a.B * a.E <= kStage)
+    hipLaunchKernelGGL(reuse_gate_kernel<true>, dim3(1), dim3(1024), 0, s, a);
+  else
+    hipLaunchKernelGGL(reuse_gate_kernel<false>, dim3(1), dim3(1024), 0, s, a);
   return hipGetLastError();
 }
 

@@ -10,7 +10,12 @@ constexpr int kMaxTopK = 16;
 constexpr int kMaxTokens = 256;
 constexpr int kMaxExperts = 256;
 
-enum : uint32_t { kPrefActivatedOnly = 1u, kBiasAbsolute = 2u, kGateFromBiased = 4u };
+enum : uint32_t {
+  kPrefActivatedOnly = 1u,
+  kBiasAbsolute = 2u,
+  kGateFromBiased = 4u,
+  kPackedWeights = 8u
+};
 enum WeightFormat : int { kWF32 = 0, kWBf16 = 1, kWQ4 = 2 };
 
 struct RouteArgs {
@@ -62,6 +67,7 @@ struct FfnArgs {
   void* hh;  // workspace: SwiGLU activations [B*k + S*B, ldh] (fp32, bf16 or fp16)
   int ldh;
   void* x16;  // workspace, int4 weights only: x as fp16 [B, H] in decode order
+  bool packed;  // weights in the packed tile order (pack.hip)
   float* out;  // [B*k + S*B, H]
 };
 
@@ -72,7 +78,17 @@ struct CombineArgs {
   int B, H, k, S;
 };
 
+struct PackArgs {
+  const void* src;
+  const void* src_s;
+  void* dst;
+  void* dst_s;
+  int n, rows, K;
+  bool q4;
+};
+
 hipError_t launch_route(const RouteArgs& a, hipStream_t s);
+hipError_t launch_pack(const PackArgs& a, hipStream_t s);
 hipError_t launch_reuse_gate(const GateArgs& a, hipStream_t s);
 hipError_t launch_ffn(const FfnArgs& a, hipStream_t s);
 hipError_t launch_ffn_bf16(const FfnArgs& a, hipStream_t s);

@@ -28,6 +28,22 @@ def weights_to_device(experts: dict, shared: dict | None, device="cuda"):
     return (dev_e, dev_s), _lib.make_weights(dev_e, dev_s)
 
 
+def pack_expert_weights(dev: tuple, wdt: str):
+    """(device tensors, Weights struct) of the packed copies of the device
+    weights `dev` = (routed dict, shared dict) from weights_to_device; use
+    them with a layer whose flags include PACKED_WEIGHTS."""
+    out = []
+    for d in dev:
+        p = {}
+        for n in ("gate", "up", "down"):
+            if n in d:
+                p[n], sc = _lib.pack_weights(wdt, d[n], d.get(n + "_s"))
+                if sc is not None:
+                    p[n + "_s"] = sc
+        out.append(p)
+    return (out[0], out[1]), _lib.make_weights(out[0], out[1])
+
+
 class VerifyPass:
     """Buffers and calls of one verify-MoE layer pass for B draft tokens."""
 

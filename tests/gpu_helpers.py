@@ -37,20 +37,25 @@ def make_inputs(shape, B, seed, rho=0.5, router_std=None, alphas=None, layer=0, 
     return d
 
 
-def run_gpu(shape, d, dev_weights=None):
-    """One pass through the C ABI; returns (host results, device weights)."""
+def run_gpu(shape, d, dev_weights=None, packed=False):
+    """One pass through the C ABI; returns (host results, device weights).
+    With packed=True the weights are re-laid by s2moe_pack_weights first and
+    the layer carries S2MOE_PACKED_WEIGHTS (dev_weights are then the packed
+    ones)."""
     import torch
 
     import paper_2608_15018_amd as s2
 
     B = d["x"].shape[0]
-    L = s2.make_layer(shape)
+    L = s2.make_layer(shape, flags=shape.flags | (s2.PACKED_WEIGHTS if packed else 0))
     p = s2.VerifyPass(L, B)
     x = s2.to_device(d["x"])
     router = s2.to_device(d["router"])
     conf = s2.to_device(d["conf_w"])
     if dev_weights is None:
         dev_weights = s2.weights_to_device(d["experts"], d["shared"])
+        if packed:
+            dev_weights = s2.pack_expert_weights(dev_weights[0], shape.wdt)
     p(x, router, conf, dev_weights[1])
     torch.cuda.synchronize()
     return p.results(), dev_weights

@@ -62,7 +62,7 @@ def _route_status(lib, layer, B=4, ptrs=True):
     ({"cap": 9}, 4, _lib.EINVAL, "cap"),
     ({"alpha": -1.0}, 4, _lib.EINVAL, "alpha"),
     ({"alpha": float("inf")}, 4, _lib.EINVAL, "alpha"),
-    ({"flags": 8}, 4, _lib.EINVAL, "flags"),
+    ({"flags": 16}, 4, _lib.EINVAL, "flags"),
     ({"n_shared": 2, "ffn_shared": 0}, 4, _lib.EINVAL, "ffn_shared"),
     ({"n_shared": 9, "ffn_shared": 64}, 4, _lib.EUNSUPPORTED, "n_shared"),
     ({"act": "f32", "wdt": "bf16"}, 4, _lib.EUNSUPPORTED, "supported"),
@@ -121,3 +121,32 @@ def test_binding_raises_with_message():
     with pytest.raises(s2.S2moeError) as ei:
         s2.workspace_bytes(_layer(top_k=0), 4)
     assert ei.value.status == _lib.EINVAL
+
+
+@pytest.mark.parametrize("args,status,needle", [
+    ((0, 1, 16, 32), _lib.EUNSUPPORTED, "w_dtype"),
+    ((5, 1, 16, 32), _lib.EINVAL, "w_dtype"),
+    ((1, 0, 16, 32), _lib.EINVAL, "n_mats"),
+    ((1, 1, 24, 32), _lib.EINVAL, "rows"),
+    ((1, 1, 16, 48), _lib.EINVAL, "cols"),
+    ((2, 1, 16, 64), _lib.EINVAL, "cols"),
+])
+def test_pack_weights_rejects_bad_shapes(lib, args, status, needle):
+    fake, other = ctypes.c_void_p(0x100000), ctypes.c_void_p(0x9000000)
+    st = lib.s2moe_pack_weights(*args, fake, fake, other, other, None)
+    assert st == status
+    assert needle in _lib.last_error()
+
+
+def test_pack_weights_rejects_overlap_and_missing_scales(lib):
+    a, b = ctypes.c_void_p(0x100000), ctypes.c_void_p(0x100400)
+    assert lib.s2moe_pack_weights(1, 1, 16, 64, a, None, b, None, None) == _lib.EINVAL
+    assert "overlap" in _lib.last_error()
+    far = ctypes.c_void_p(0x9000000)
+    assert lib.s2moe_pack_weights(2, 1, 16, 128, a, None, far, None, None) == _lib.EINVAL
+    assert "src_scales" in _lib.last_error()
+
+
+def test_packed_flag_needs_16bit_or_int4_weights(lib):
+    st, msg = _route_status(lib, _layer(act="f32", wdt="f32", flags=8))
+    assert st == _lib.EUNSUPPORTED and "PACKED" in msg

@@ -183,6 +183,73 @@ def test_exact_ties_resolved_by_lower_index():
         assert np.abs(got["gate_w"] - ref["gate_w"]).max() <= 1e-6
 
 
+# ---------------------------------------------------------------- packed weights
+def _expected_pack_bf16(m):
+    """Reference tile order written out independently: tile (rt, s) of 16 rows
+    x 32 columns, lane L -> row 16 rt + L % 16, columns 32 s + 8 (L // 16)."""
+    n, rows, K = m.shape
+    out = np.empty(m.size, dtype=m.dtype)
+    pos = 0
+    for i in range(n):
+        for rt in range(rows // 16):
+            for s in range(K // 32):
+                for L in range(64):
+                    r, c = 16 * rt + L % 16, 32 * s + 8 * (L // 16)
+                    out[pos:pos + 8] = m[i, r, c:c + 8]
+                    pos += 8
+    return out.reshape(m.shape)
+
+
+def _expected_pack_q4(codes, scales):
+    n, rows, half = codes.shape
+    K = 2 * half
+    oc = np.empty(codes.size, dtype=codes.dtype)
+    osc = np.empty(scales.size, dtype=scales.dtype)
+    pc = ps = 0
+    for i in range(n):
+        for rt in range(rows // 16):
+            for S in range(K // 128):
+                for L in range(64):
+                    r, g = 16 * rt + L % 16, 4 * S + L // 16
+                    oc[pc:pc + 16] = codes[i, r, 16 * g:16 * g + 16]
+                    osc[ps] = scales[i, r, g]
+                    pc += 16
+                    ps += 1
+    return oc.reshape(codes.shape), osc.reshape(scales.shape)
+
+
+def test_pack_layout():
+    import paper_2608_15018_amd as s2
+    rng = np.random.default_rng(1)
+    m = rng.integers(0, 1 << 16, size=(2, 32, 96), dtype=np.uint16)
+    got, _ = s2.pack_weights("bf16", s2.to_device(m))
+    torch.cuda.synchronize()
+    got = got.view(torch.int16).cpu().numpy().view(np.uint16)
+    np.testing.assert_array_equal(got, _expected_pack_bf16(m))
+    codes = rng.integers(0, 256, size=(2, 32, 128), dtype=np.uint8)
+    scales = rng.standard_normal((2, 32, 8)).astype(np.float16)
+    gc, gs = s2.pack_weights("q4g32", s2.to_device(codes), s2.to_device(scales))
+    torch.cuda.synchronize()
+    ec, es = _expected_pack_q4(codes, scales)
+    np.testing.assert_array_equal(gc.cpu().numpy(), ec)
+    np.testing.assert_array_equal(gs.cpu().numpy(), es)
+
+
+@pytest.mark.parametrize("name", ["c2s", "c3s", "c4s", "c5s"])
+def test_packed_weights_match_plain_bitwise(name):
+    """The packed layout changes only where weights are read from: the MFMA
+    sequence, hence every output bit, is the same as with plain weights."""
+    shape, B, rho, rstd = SMALL[name]
+    d = make_inputs(shape, B, seed=404, rho=rho, router_std=rstd)
+    plain, _ = run_gpu(shape, d)
+    packed, _ = run_gpu(shape, d, packed=True)
+    for n in ("idx", "slot", "uniq"):
+        np.testing.assert_array_equal(packed[n], plain[n])
+    assert np.array_equal(packed["expert_out"], plain["expert_out"]), name
+    assert np.array_equal(packed["y"], plain["y"]), name
+    check_outputs(packed, _oracle(shape, d), shape.wdt, name + " packed")
+
+
 # ---------------------------------------------------------------- full sizes
 def _workload_inputs(name, B, seed, layer=0, alphas=None):
     wl = WORKLOADS[name]
@@ -196,6 +263,10 @@ def test_full_c2_mixtral_bf16():
     d = _workload_inputs("c2", 16, seed=1)
     got, ref = _full_check(wl.shape, d, "c2 full")
     log(f"[parity] c2 reuse ratio {ref['reuse_ratio']:.3f}")
+    packed, _ = run_gpu(wl.shape, d, packed=True)
+    check_routing(packed, ref, "c2 full packed")
+    errs = check_outputs(packed, ref, "bf16", "c2 full packed")
+    log(f"[parity] c2 full packed ok errs={errs}")
 
 
 def test_full_c3_alpha_sweep():
@@ -243,6 +314,9 @@ def test_full_c5_int4_layers():
         dw, deq = cache[layer]
         log(f"[parity] c5 layer={layer} B={B}")
         got, _ = run_gpu(sh, d, dw)
+        if B == 16:
+            packed, _ = run_gpu(sh, d, packed=True)
+            assert np.array_equal(packed["expert_out"], got["expert_out"])
         ref = oracle.forward(d["x"], d["router"], d["conf_w"], deq, {}, sh.with_(wdt="f32"))
         check_routing(got, ref, f"c5 l={layer} B={B}")
         errs = check_outputs(got, ref, "q4g32", f"c5 l={layer} B={B}")
