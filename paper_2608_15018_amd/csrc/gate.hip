@@ -5,44 +5,53 @@
 // One workgroup of 16 waves handles the whole verify batch (B <= 256,
 // E <= 256): the decisions couple all tokens through g, and the batch is
 // small.  Nothing here is a serial loop over assignments:
-//   * g: one thread per expert sums w_b * ell_{b,e} over b in order;
-//   * TopCap: each expert's rank among the candidates by (g desc, id asc);
-//   * per token (one wave): biased order keys, a bitwise threshold search
-//     for the k-th largest value (ties to the lower expert id), ballot ranks
-//     for ascending-id order, DPP softmax;
+//   * g: a few threads per expert sum runs of tokens, runs added in order;
+//   * TopCap: each expert's rank among the candidates by (g desc, id asc),
+//     its comparisons split over several threads;
+//   * per token (one wave, up to 4 tokens at a time): biased order keys, an
+//     exact top-k (a bitwise threshold search over the upper key halves,
+//     then the boundary bucket ranked; ties to the lower expert id), ballot
+//     ranks for ascending-id order, DPP softmax;
 //   * buckets: a B-bit token mask per expert (LDS 64-bit ORs), so an
 //     assignment's position in its expert's list is the popcount of the mask
 //     below its token.
 // Every result is deterministic: integer atomics only (bitwise OR), fixed
 // floating-point summation orders, rank-based placement.
-#include "common.h"
 #include "kernels.h"
+#include "select.h"
 
 namespace s2moe {
 
 constexpr int kStage = 10240;  // logits staged in LDS up to B * E = 10240
+constexpr float kLog2e = 1.4426950408889634f;
 
-template <bool kStaged>
+// kNJ = expert slots per lane (E <= 64 kNJ); kNT = tokens a wave takes
+// through the threshold search together.
+template <bool kStaged, int kNJ, int kNT>
 __global__ __launch_bounds__(1024) void reuse_gate_kernel(GateArgs a) {
   constexpr int kMaskWords = kMaxTokens / 64;
   __shared__ float ell_s[kStaged ? kStage : 1];
   __shared__ float w_s[kMaxTokens];
   __shared__ float gap_s[kMaxTokens];
-  __shared__ __align__(16) float gm_s[kMaxExperts];  // g of candidates, -inf otherwise
+  __shared__ float gm_s[kMaxExperts];                  // g of candidates, -inf otherwise
+  __shared__ int rank_s[kMaxExperts];
   __shared__ int pref_s[kMaxExperts];
   __shared__ int count_s[kMaxExperts];
   __shared__ int offset_s[kMaxExperts + 1];
   __shared__ uint64_t mask_s[kMaxExperts][kMaskWords];
-  __shared__ uint8_t idx_s[kMaxTokens * kMaxTopK];
+  // [part][E] partial sums of g first, the selected expert ids later.
+  static_assert(kMaxTokens * kMaxTopK == 4 * 1024, "shared buffer size");
+  __shared__ float gpart_s[1024];
+  uint8_t* idx_s = reinterpret_cast<uint8_t*>(gpart_s);
   __shared__ int cand_s[kMaxExperts];
 
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
-  const int wave = tid >> 6;
+  const int wave = wave_id();
   const int n_waves = blockDim.x >> 6;
   const int B = a.B, E = a.E, k = a.k;
 
-  // Non-negative confidences w_b; logits to LDS; cleared masks.
+  // Non-negative confidences w_b; logits to LDS; cleared masks and ranks.
   int positive = 0;
   if (tid < B) {
     const float w = fmaxf(a.conf_w[tid], 0.f);
@@ -67,7 +76,10 @@ __global__ __launch_bounds__(1024) void reuse_gate_kernel(GateArgs a) {
   }
   for (int i = tid; i < kMaxExperts * kMaskWords; i += blockDim.x)
     (&mask_s[0][0])[i] = 0ull;
-  if (tid < kMaxExperts) cand_s[tid] = (!(a.flags & kPrefActivatedOnly) && tid < E) ? 1 : 0;
+  if (tid < kMaxExperts) {
+    cand_s[tid] = (!(a.flags & kPrefActivatedOnly) && tid < E) ? 1 : 0;
+    rank_s[tid] = 0;
+  }
   const int active = __syncthreads_or(positive);
   const float* ell = kStaged ? static_cast<const float*>(ell_s) : a.logits;
 
@@ -77,86 +89,108 @@ __global__ __launch_bounds__(1024) void reuse_gate_kernel(GateArgs a) {
       const int e = a.plain_idx[i];
       if (e >= 0 && e < E) cand_s[e] = 1;
     }
-    __syncthreads();
   }
 
-  // g_e = sum_b w_b * ell_{b,e}, summed over b in order.
-  if (tid < E) {
+  // g_e = sum_b w_b * ell_{b,e}: `parts` threads per expert each sum a
+  // contiguous run of tokens in order, then the runs are added in order.
+  int parts = 1;
+  while (parts * 2 * E <= 1024 && parts * 2 <= B) parts *= 2;
+  const int run = (B + parts - 1) / parts;
+  if (tid < parts * E) {
+    const int e = tid % E, part = tid / E;
+    const int b_lo = part * run, b_hi = min(B, b_lo + run);
     float s = 0.f;
-#pragma unroll 8
-    for (int b = 0; b < B; ++b) s = fmaf(w_s[b], ell[(size_t)b * E + tid], s);
+#pragma unroll 4
+    for (int b = b_lo; b < b_hi; ++b) s = fmaf(w_s[b], ell[(size_t)b * E + e], s);
+    gpart_s[part * E + e] = s;
+  }
+  __syncthreads();
+  if (tid < E) {
+    float s = gpart_s[tid];
+    for (int part = 1; part < parts; ++part) s += gpart_s[part * E + tid];
     a.g[tid] = s;
     gm_s[tid] = cand_s[tid] ? s : -INFINITY;
   }
   __syncthreads();
 
-  // E* = TopCap(g): rank of each candidate by (g desc, id asc).
+  // E* = TopCap(g): rank of each expert by (g desc, id asc); non-candidates
+  // hold -inf and so rank after every candidate.
+  if (active) {
+    block_rank_desc(gm_s, E, rank_s, tid, blockDim.x);
+    __syncthreads();
+  }
   if (tid < E) {
-    int p = 0;
-    if (active && cand_s[tid]) {
-      const float ge = gm_s[tid];
-      int rank = 0;
-      const f32x4* g4 = reinterpret_cast<const f32x4*>(gm_s);
-      for (int q = 0; q < (E + 3) / 4; ++q) {
-        const f32x4 g2 = g4[q];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int e2 = 4 * q + i;
-          rank += (e2 < E) && ((g2[i] > ge) || (g2[i] == ge && e2 < tid));
-        }
-      }
-      p = rank < a.cap;
-    }
+    const int p = active && cand_s[tid] && rank_s[tid] < a.cap;
     pref_s[tid] = p;
     a.pref[tid] = p;
   }
   __syncthreads();
 
   // Per token: lambda_b, biased keys, biased top-k, gate weights, masks.
+  // Wave w takes tokens w, w + 16, ...; kNT of them at a time.
   const bool from_biased = (a.flags & kGateFromBiased) != 0;
-  for (int b = wave; b < B; b += n_waves) {
-    float lam = 0.f;
-    if (active) lam = (a.flags & kBiasAbsolute) ? a.alpha : a.alpha * gap_s[b];
-    float l[4], lb[4];
-    uint32_t key[4];
+  for (int b0 = wave; b0 < B; b0 += n_waves * kNT) {
+    float l[kNT][kNJ], lb[kNT][kNJ];
+    uint32_t key[kNT][kNJ];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int e = lane + kWave * j;
-      l[j] = 0.f;
-      lb[j] = 0.f;
-      key[j] = 0;
-      if (e < E) {
-        l[j] = ell[(size_t)b * E + e];
-        lb[j] = pref_s[e] ? l[j] + lam : l[j];
-        key[j] = order_key(lb[j]);
+    for (int t = 0; t < kNT; ++t) {
+      const int b = b0 + t * n_waves;
+      float lam = 0.f;
+      if (active && b < B) lam = (a.flags & kBiasAbsolute) ? a.alpha : a.alpha * gap_s[b];
+#pragma unroll
+      for (int j = 0; j < kNJ; ++j) {
+        const int e = lane + kWave * j;
+        l[t][j] = 0.f;
+        lb[t][j] = 0.f;
+        key[t][j] = 0;
+        if (b < B && e < E) {
+          l[t][j] = ell[(size_t)b * E + e];
+          lb[t][j] = pref_s[e] ? l[t][j] + lam : l[t][j];
+          key[t][j] = order_key(lb[t][j]);
+        }
       }
     }
-    const uint32_t bits = wave_select_top(key, wave_kth_key(key, k), k);
-    float m = -INFINITY;
+    uint32_t bits[kNT];
+    wave_top_k<kNT, kNJ>(key, k, bits);
+    // Softmax over the selected k: max through the order keys (exact),
+    // then exp, a DPP sum and one reciprocal.
+    float ez[kNT][kNJ], s[kNT], inv_s[kNT];
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
-      if ((bits >> j) & 1u) m = fmaxf(m, from_biased ? lb[j] : l[j]);
-    int rank[4];
-    wave_rank_flagged(bits, rank);
-    m = wave_max_dpp(m);
-    float ez[4];
-    float s = 0.f;
+    for (int t = 0; t < kNT; ++t) {
+      uint32_t mk = 0;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      ez[j] = ((bits >> j) & 1u) ? expf((from_biased ? lb[j] : l[j]) - m) : 0.f;
-      s += ez[j];
+      for (int j = 0; j < kNJ; ++j)
+        if ((bits[t] >> j) & 1u) mk = max(mk, from_biased ? key[t][j] : order_key(l[t][j]));
+      const float m = key_value(wave_max_key_dpp(mk));
+      s[t] = 0.f;
+#pragma unroll
+      for (int j = 0; j < kNJ; ++j) {
+        // exp(x - m) as 2^((x - m) log2 e) on the hardware exp2 (about 1e-6
+        // relative error for |x - m| < 20)
+        const float x = from_biased ? lb[t][j] : l[t][j];
+        ez[t][j] = ((bits[t] >> j) & 1u) ? __builtin_amdgcn_exp2f((x - m) * kLog2e) : 0.f;
+        s[t] += ez[t][j];
+      }
     }
-    s = wave_sum_dpp(s);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      if ((bits >> j) & 1u) {
-        const int pos = b * k + rank[j];
-        const int e = lane + kWave * j;
-        a.idx[pos] = e;
-        a.gate_w[pos] = ez[j] / s;
-        idx_s[pos] = (uint8_t)e;
-        atomicOr(reinterpret_cast<unsigned long long*>(&mask_s[e][b >> 6]),
-                 1ull << (b & 63));
+    for (int t = 0; t < kNT; ++t) inv_s[t] = __builtin_amdgcn_rcpf(wave_sum_dpp(s[t]));
+#pragma unroll
+    for (int t = 0; t < kNT; ++t) {
+      const int b = b0 + t * n_waves;
+      if (b >= B) break;
+      int rank[kNJ];
+      wave_rank_flagged<kNJ>(bits[t], rank);
+#pragma unroll
+      for (int j = 0; j < kNJ; ++j) {
+        if ((bits[t] >> j) & 1u) {
+          const int pos = b * k + rank[j];
+          const int e = lane + kWave * j;
+          a.idx[pos] = e;
+          a.gate_w[pos] = ez[t][j] * inv_s[t];
+          idx_s[pos] = (uint8_t)e;
+          atomicOr(reinterpret_cast<unsigned long long*>(&mask_s[e][b >> 6]),
+                   1ull << (b & 63));
+        }
       }
     }
   }
@@ -181,9 +215,11 @@ __global__ __launch_bounds__(1024) void reuse_gate_kernel(GateArgs a) {
       sum_c += c[j];
       sum_f += f[j];
     }
-    int total_c, total_f;
-    int run_c = wave_exclusive_scan(sum_c, &total_c);
-    int run_f = wave_exclusive_scan(sum_f, &total_f);
+    const int incl_c = wave_inclusive_scan_dpp(sum_c);
+    const int incl_f = wave_inclusive_scan_dpp(sum_f);
+    const int total_c = __builtin_amdgcn_readlane(incl_c, 63);
+    const int total_f = __builtin_amdgcn_readlane(incl_f, 63);
+    int run_c = incl_c - sum_c, run_f = incl_f - sum_f;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int e = lane * 4 + j;
@@ -220,11 +256,31 @@ __global__ __launch_bounds__(1024) void reuse_gate_kernel(GateArgs a) {
   }
 }
 
+template <bool kStaged, int kNJ>
+void launch_gate_nj(const GateArgs& a, hipStream_t s) {
+  if (a.B <= 16)
+    hipLaunchKernelGGL((reuse_gate_kernel<kStaged, kNJ, 1>), dim3(1), dim3(1024), 0, s, a);
+  else if (a.B <= 32)
+    hipLaunchKernelGGL((reuse_gate_kernel<kStaged, kNJ, 2>), dim3(1), dim3(1024), 0, s, a);
+  else
+    hipLaunchKernelGGL((reuse_gate_kernel<kStaged, kNJ, 4>), dim3(1), dim3(1024), 0, s, a);
+}
+
+template <bool kStaged>
+void launch_gate_staged(const GateArgs& a, hipStream_t s) {
+  if (a.E <= 64)
+    launch_gate_nj<kStaged, 1>(a, s);
+  else if (a.E <= 128)
+    launch_gate_nj<kStaged, 2>(a, s);
+  else
+    launch_gate_nj<kStaged, 4>(a, s);
+}
+
 hipError_t launch_reuse_gate(const GateArgs& a, hipStream_t s) {
   if (a.B * a.E <= kStage)
-    hipLaunchKernelGGL(reuse_gate_kernel<true>, dim3(1), dim3(1024), 0, s, a);
+    launch_gate_staged<true>(a, s);
   else
-    hipLaunchKernelGGL(reuse_gate_kernel<false>, dim3(1), dim3(1024), 0, s, a);
+    launch_gate_staged<false>(a, s);
   return hipGetLastError();
 }
 

@@ -1,25 +1,26 @@
 // Router logits and plain top-(k+1) per draft token (Sec. "Reuse-aware
 // Expert Gating": target gating logits ell_b; gap_b = ell_(1) - ell_(k+1)).
 //
-// One workgroup of up to 16 waves per token.  Each wave takes 4 experts per
-// pass; the lanes split H in 16-byte chunks (the token row and 4 router rows
-// read coalesced, all in flight together) and DPP reductions add the lane
-// partials in a fixed order.  Wave 0 then ranks the E logits with a bitwise
-// threshold search for the (k+1)-th largest value.
-#include "common.h"
+// One workgroup of up to 16 waves per token.  A wave takes 4 experts and a
+// slice of H per item (H is sliced when there are few experts, so that all
+// waves load at once); its lanes split the slice in 16-byte chunks (the
+// token row and 4 router rows read coalesced, all in flight together), DPP
+// reductions add the lane partials and the slices are summed in order.  The workgroup then ranks the E logits (each
+// rank counted by several threads) and wave 0 lists the plain top-k.
 #include "kernels.h"
+#include "select.h"
 
 namespace s2moe {
 
 namespace {
 
-// Dot products of the token row with 4 router rows (e0 .. e0+3, those < E):
-// lanes split H in 16-byte chunks, so each iteration has 5 loads in flight.
+// Partial dot products of the token row with 4 router rows (e0 .. e0+3,
+// those < E) over the 16-byte chunks [c_lo, c_hi) of H: lanes split the
+// chunks, so up to 4 iterations x 5 loads are in flight together.
 template <bool kBf16>
 __device__ __forceinline__ void dot_rows4(const char* x, const char* w, int H, int e0, int E,
-                                          int lane, float acc[4]) {
+                                          int c_lo, int c_hi, int lane, float acc[4]) {
   const size_t row = (size_t)H * (kBf16 ? 2 : 4);
-  const int n = H / (kBf16 ? 8 : 4);
   const u32x4* xr = reinterpret_cast<const u32x4*>(x);
   const u32x4* wr[4];
 #pragma unroll
@@ -27,8 +28,8 @@ __device__ __forceinline__ void dot_rows4(const char* x, const char* w, int H, i
     acc[q] = 0.f;
     wr[q] = reinterpret_cast<const u32x4*>(w + (size_t)min(e0 + q, E - 1) * row);
   }
-#pragma unroll 2
-  for (int c = lane; c < n; c += kWave) {
+#pragma unroll 4
+  for (int c = c_lo + lane; c < c_hi; c += kWave) {
     const u32x4 xc = xr[c];
     u32x4 wc[4];
 #pragma unroll
@@ -52,62 +53,86 @@ __device__ __forceinline__ void dot_rows4(const char* x, const char* w, int H, i
   for (int q = 0; q < 4; ++q) acc[q] = wave_sum_dpp(acc[q]);
 }
 
+// Number of H slices: as many as keep every wave busy (slices x expert
+// groups <= 16) while each slice still spans at least 64 chunks.
+__host__ __device__ inline int route_slices(int E, int chunks) {
+  const int groups = (E + 3) / 4;
+  int S = 1;
+  while (S * 2 * groups <= 16 && chunks / (S * 2) >= kWave) S *= 2;
+  return S;
+}
+
 template <bool kBf16>
 __global__ __launch_bounds__(1024) void route_kernel(RouteArgs a) {
+  __shared__ float part_s[kMaxExperts];  // [slice][E]: slices * E <= 256
   __shared__ float ell_s[kMaxExperts];
-  const int lane = threadIdx.x & (kWave - 1);
-  const int wave = threadIdx.x >> 6;
+  __shared__ int rank_s[kMaxExperts];
+  __shared__ float top1_s, kth1_s;
+  const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1);
+  const int wave = wave_id();
   const int n_waves = blockDim.x >> 6;
   const int b = blockIdx.x;
   const int H = a.H, E = a.E, k = a.k;
   const char* xb = static_cast<const char*>(a.x) + (size_t)b * H * (kBf16 ? 2 : 4);
   const char* wr = static_cast<const char*>(a.router);
+  const int chunks = H / (kBf16 ? 8 : 4);
+  const int groups = (E + 3) / 4;
+  const int S = route_slices(E, chunks);
+  const int per_slice = (chunks + S - 1) / S;
 
-  for (int e0 = wave * 4; e0 < E; e0 += n_waves * 4) {
+  if (tid < E) rank_s[tid] = 0;
+  // Work item p = (slice, group of 4 experts), p = slice * groups + group.
+  for (int p = wave; p < S * groups; p += n_waves) {
+    const int slice = p / groups, e0 = (p - slice * groups) * 4;
+    const int c_lo = slice * per_slice, c_hi = min(chunks, c_lo + per_slice);
     float l[4];
-    dot_rows4<kBf16>(xb, wr, H, e0, E, lane, l);
+    dot_rows4<kBf16>(xb, wr, H, e0, E, c_lo, c_hi, lane, l);
     if (lane == 0) {
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        if (e0 + q < E) {
-          ell_s[e0 + q] = l[q];
-          a.logits[(size_t)b * E + e0 + q] = l[q];
-        }
-      }
+      for (int q = 0; q < 4; ++q)
+        if (e0 + q < E) part_s[slice * E + e0 + q] = l[q];
     }
   }
   __syncthreads();
+  if (tid < E) {
+    float v = part_s[tid];
+    for (int sl = 1; sl < S; ++sl) v += part_s[sl * E + tid];
+    ell_s[tid] = v;
+    a.logits[(size_t)b * E + tid] = v;
+  }
+  __syncthreads();
+  // Rank of every logit (value desc, expert id asc); the plain top-k are
+  // ranks 0..k-1 and ell_(k+1) is the value of rank k.
+  block_rank_desc(ell_s, E, rank_s, tid, blockDim.x);
+  __syncthreads();
+  if (tid < E) {
+    if (rank_s[tid] == 0) top1_s = ell_s[tid];
+    if (rank_s[tid] == k) kth1_s = ell_s[tid];
+  }
+  __syncthreads();
   if (wave != 0) return;
-
-  uint32_t key[4];
-  float vmax = -INFINITY;
+  uint32_t bits = 0;
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const int e = lane + kWave * j;
-    key[j] = 0;
-    if (e < E) {
-      const float v = ell_s[e];
-      key[j] = order_key(v);
-      vmax = fmaxf(vmax, v);
-    }
+    if (e < E && rank_s[e] < k) bits |= 1u << j;
   }
-  // ell_(k+1) is the (k+1)-th largest value; the plain top-k are the k best
-  // entries, which all rank at or above it.
-  const uint32_t kth1 = wave_kth_key(key, k + 1);
-  const float top1 = wave_max_dpp(vmax);
-  const uint32_t bits = wave_select_top(key, kth1, k);
   int rank[4];
-  wave_rank_flagged(bits, rank);
+  wave_rank_flagged<4>(bits, rank);
 #pragma unroll
   for (int j = 0; j < 4; ++j)
     if ((bits >> j) & 1u) a.plain_idx[(size_t)b * k + rank[j]] = lane + kWave * j;
-  if (lane == 0) a.gap[b] = top1 - key_value(kth1);
+  if (lane == 0) a.gap[b] = top1_s - kth1_s;
 }
 
 }  // namespace
 
 hipError_t launch_route(const RouteArgs& a, hipStream_t s) {
-  const int waves = min(16, (a.E + 3) / 4);  // 4 experts per wave and pass
+  // One wave per (H slice, 4 experts) item, at most 16; E <= 256 keeps at
+  // least one thread per expert for the ranking.
+  const int chunks = a.H / (a.bf16 ? 8 : 4);
+  const int waves = min(16, route_slices(a.E, chunks) * ((a.E + 3) / 4));
   const dim3 block(64 * waves);
   if (a.bf16)
     hipLaunchKernelGGL(route_kernel<true>, dim3(a.B), block, 0, s, a);
