@@ -12,8 +12,8 @@ import pytest
 
 import oracle
 from synth.configs import WORKLOAD_ID, WORKLOADS, LayerShape
-from tests.gpu_helpers import (check_outputs, check_routing, log, make_inputs, rel_err,
-                               run_gpu)
+from tests.gpu_helpers import (TOL_GATE_W, check_outputs, check_routing, log, make_inputs,
+                               rel_err, run_gpu)
 
 pytestmark = pytest.mark.gpu
 
@@ -181,6 +181,48 @@ def test_exact_ties_resolved_by_lower_index():
             np.testing.assert_array_equal(got[n], ref[n], err_msg=f"{n} alpha={alpha} f={flags}")
         np.testing.assert_array_equal(got["g"], ref["g"].astype(np.float32))
         assert np.abs(got["gate_w"] - ref["gate_w"]).max() <= 1e-6
+
+
+@pytest.mark.parametrize("B,E,k,cap", [(16, 8, 2, 4), (32, 128, 8, 14), (64, 64, 6, 16),
+                                       (200, 256, 16, 40)])
+def test_near_ties_sharing_upper_key_bits(B, E, k, cap):
+    """Logits +-(1 + c 2^-16) with c < 96 all share the upper 16 bits of
+    their order keys, so every top-k boundary falls inside one radix bucket
+    and is settled by the exact in-bucket ranking; codes repeat, so exact
+    ties occur too.  Weights are 0/1 and alpha is dyadic, so g, the bias
+    and the biased logits are exact in fp32 and fp64.  Route runs on x with
+    a one-hot fp32 router (logits = x exactly), then reuse_gate."""
+    import paper_2608_15018_amd as s2
+    rng = np.random.default_rng(B * 1000 + E)
+    codes = rng.integers(0, 96, size=(B, E))
+    sign = np.where(rng.random((B, E)) < 0.3, -1.0, 1.0)
+    ell = sign * (1.0 + codes * 2.0 ** -16)
+    H = max(64, -(-E // 64) * 64)
+    x = np.zeros((B, H), np.float32)
+    x[:, :E] = ell
+    router = np.zeros((E, H), np.float32)
+    router[np.arange(E), np.arange(E)] = 1.0
+    w = (rng.random(B) < 0.6).astype(np.float32)
+    w[0] = 1.0
+    r_ref = oracle.route(x, router, k, "f32")
+    for alpha, flags in ((0.5, 0), (1.0, 4), (0.5, 1)):
+        ref = oracle.reuse_gate(r_ref["logits"], r_ref["gap"], r_ref["plain_idx"], w, k, cap,
+                                alpha, flags)
+        L = s2.make_layer(hidden=H, ffn=64, n_experts=E, top_k=k, cap=cap, alpha=alpha,
+                          flags=flags, act="f32", wdt="f32")
+        rt = s2.Routing(L, B)
+        s2.route(L, torch.from_numpy(x).cuda(), torch.from_numpy(router).cuda(), rt)
+        s2.reuse_gate(L, torch.from_numpy(w).cuda(), rt)
+        torch.cuda.synchronize()
+        got = rt.host()
+        label = f"B={B} E={E} alpha={alpha} flags={flags}"
+        np.testing.assert_array_equal(got["logits"], ell.astype(np.float32), err_msg=label)
+        np.testing.assert_array_equal(got["plain_idx"], r_ref["plain_idx"], err_msg=label)
+        np.testing.assert_array_equal(got["gap"], r_ref["gap"].astype(np.float32), err_msg=label)
+        for n in ("pref", "idx", "count", "offset", "slot", "uniq"):
+            np.testing.assert_array_equal(got[n], ref[n], err_msg=f"{n} {label}")
+        np.testing.assert_array_equal(got["g"], ref["g"].astype(np.float32), err_msg=label)
+        assert np.abs(got["gate_w"] - ref["gate_w"]).max() <= TOL_GATE_W, label
 
 
 # ---------------------------------------------------------------- packed weights
