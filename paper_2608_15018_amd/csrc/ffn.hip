@@ -26,7 +26,7 @@ __global__ __launch_bounds__(256) void ffn_f32_kernel(FfnArgs a) {
   int rb;
   if (!resolve_block(a, kMode, 4, &seg, &rb)) return;
   const int lane = threadIdx.x & (kWave - 1);
-  const int row = rb * 4 + (threadIdx.x >> 6);
+  const int row = rb * 4 + wave_id();
   const int rows = kMode == 0 ? (seg.shared ? a.Fs : a.F) : a.H;
   const int K = kMode == 0 ? a.H : (seg.shared ? a.Fs : a.F);
   const float* W0;

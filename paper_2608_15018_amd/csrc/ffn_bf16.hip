@@ -77,7 +77,7 @@ __device__ __forceinline__ void unit_pass(const FfnArgs& a, const Segment& seg, 
                                           f32x4* red) {
   constexpr int NM = kMode == 0 ? 2 : 1;
   const int lane = threadIdx.x & (kWave - 1);
-  const int wave = threadIdx.x >> 6;
+  const int wave = wave_id();
   const int rA = lane & 15, gK = lane >> 4;
   const int nks = K / 32;
   const int lo = wave * nks / W, hi = (wave + 1) * nks / W;
@@ -112,16 +112,10 @@ __device__ __forceinline__ void unit_pass(const FfnArgs& a, const Segment& seg, 
 #pragma unroll
       for (int tt = 0; tt < T; ++tt) acc[m][r][tt] = f32x4{0.f, 0.f, 0.f, 0.f};
   if (hi > lo) {
-    const int nch = (hi - lo + U - 1) / U;
-    Stage<T, R, NM, U> st0, st1;
-    load_stage<kPacked>(st0, pa, xb, lo, hi);
-    for (int c = 0; c < nch; c += 2) {
-      if (c + 1 < nch) load_stage<kPacked>(st1, pa, xb, lo + (c + 1) * U, hi);
-      compute_stage(st0, acc, lo + c * U, hi);
-      if (c + 1 >= nch) break;
-      if (c + 2 < nch) load_stage<kPacked>(st0, pa, xb, lo + (c + 2) * U, hi);
-      compute_stage(st1, acc, lo + (c + 1) * U, hi);
-    }
+    pipeline2<Stage<T, R, NM, U>>(
+        (hi - lo + U - 1) / U,
+        [&](Stage<T, R, NM, U>& st, int c) { load_stage<kPacked>(st, pa, xb, lo + c * U, hi); },
+        [&](const Stage<T, R, NM, U>& st, int c) { compute_stage(st, acc, lo + c * U, hi); });
   }
 
   if (W > 1) {

@@ -77,6 +77,44 @@ __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) {
   return r;
 }
 
+// Streams n >= 1 stages: stage i + 1 is requested before stage i is
+// consumed, with two register buffers.  Every load sits on a path without
+// conditions of its own (a two-stage loop body, then a one- or two-stage
+// tail), so the compiler knows how many loads are in flight at each use and
+// waits only for the stage it needs; a load under a condition would make it
+// wait for all of them.
+// The scheduling barriers keep the compiler from sinking the next stage's
+// loads into the current stage's arithmetic.
+#ifndef S2MOE_PIPE_BARRIER
+#define S2MOE_PIPE_BARRIER 1
+#endif
+__device__ __forceinline__ void pipe_barrier() {
+  if (S2MOE_PIPE_BARRIER) __builtin_amdgcn_sched_barrier(0);
+}
+
+template <class Stage, class Load, class Use>
+__device__ __forceinline__ void pipeline2(int n, Load&& load, Use&& use) {
+  Stage a, b;
+  load(a, 0);
+  int i = 0;
+  for (; i + 2 < n; i += 2) {
+    load(b, i + 1);
+    pipe_barrier();
+    use(a, i);
+    load(a, i + 2);
+    pipe_barrier();
+    use(b, i + 1);
+  }
+  if (i + 1 < n) {
+    load(b, i + 1);
+    pipe_barrier();
+    use(a, i);
+    use(b, i + 1);
+  } else {
+    use(a, i);
+  }
+}
+
 // Number of blocks of `rows_per_block` rows over all experts a launch covers.
 inline int n_blocks(const FfnArgs& a, int mode, int rows_per_block) {
   const int rows_r = mode == 0 ? a.F : a.H;

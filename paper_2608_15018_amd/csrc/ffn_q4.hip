@@ -3,19 +3,22 @@
 //
 // A lane reads one whole 32-code group (16 bytes) of its weight row per
 // 128-wide "super-step" (lanes 16 apart take consecutive groups, so a row's
-// 64 bytes arrive in one load) plus that group's scale.  Each code dword
-// (8 codes) becomes the fp16 values 1024 + q with one and-or per pair; a
-// packed add of -1032 gives q - 8 exactly, and a packed multiply by the
-// group scale gives round_fp16(s * (q - 8)).  The four dwords are the A
-// operands of four v_mfma_f32_16x16x32_f16, accumulated in fp32, so no
-// dequantised weight is ever written to memory and no per-group epilogue is
-// needed.  The expansion yields the K order (0,4,2,6,1,5,3,7) inside each
-// 8-element block; the activations are kept in fp16 in that same order (a
-// prep kernel converts x, the gate-up epilogue writes Hh so), so the B
-// operands are plain 16-byte loads.
+// 64 bytes arrive in one load) plus that group's scale.  Each code dword (8
+// codes, nibble slots 0..7) becomes 4 fp16 pairs with one shift and four
+// and-or operations: slots (0,4) and (2,6) land in the low mantissa bits of
+// 0x6400 (the fp16 number 1024 + q), slots (1,5) and (3,7) four bits higher
+// (1024 + 16 q).  Exact packed fp16 steps take them to q - 8 (a subtract of
+// 1032, or a fused (h / 16) - 72), and a packed multiply by the group scale
+// gives round_fp16(s * (q - 8)).  The four dwords are the A operands of four
+// v_mfma_f32_16x16x32_f16, accumulated in fp32, so no dequantised weight is
+// ever written to memory and no per-group epilogue is needed.  The decode
+// yields the slot order (0,4,1,5,2,6,3,7) inside each 8-element block; the
+// activations are kept in fp16 in that same order (a prep kernel converts x,
+// the gate-up epilogue writes Hh so), with the 8-blocks of each super-step
+// stored so that every B-operand load reads 64 contiguous bytes per token.
 //
 // Work decomposition as in the bf16 kernel: R 16-row tiles per unit, W waves
-// split K, double-buffered register pipeline, LDS reduction in wave order.
+// split K, two-stage register pipeline, LDS reduction in wave order.
 #include "ffn_common.h"
 
 namespace s2moe {
@@ -37,26 +40,42 @@ __device__ __forceinline__ half8v as_half8(u32x4 v) {
   return r;
 }
 
-// Position of element e of an 8-element block in the expansion order
-// (0,4,2,6,1,5,3,7); the order is its own inverse.
-__device__ __forceinline__ int perm8(int e) {
-  return ((e & 1) << 2) | (e & 2) | ((e >> 2) & 1);
+// Position of element e of an 8-element block in the decode order
+// (0,4,1,5,2,6,3,7).
+__device__ __forceinline__ int pos8(int e) { return ((e & 3) << 1) | (e >> 2); }
+
+// Where 8-block c of a row of activations is stored: inside each 128-wide
+// super-step (16 blocks, block 4 g + j = dword j of code group g) the blocks
+// are stored j-major, so that the four lanes of one token that feed MFMA j
+// read 64 contiguous bytes.
+__host__ __device__ __forceinline__ int block_pos(int c) {
+  return (c & ~15) | ((c & 3) << 2) | ((c >> 2) & 3);
 }
 
-// 8 codes (one dword) -> s * (q - 8) as fp16, in expansion order.
-__device__ __forceinline__ half8v q4_decode(uint32_t w, half2v s2) {
+// The value unchanged but held in a register the compiler cannot see through,
+// so that "(w & mask) | magic" becomes one v_and_or_b32 (a VOP3 instruction
+// takes at most one literal).
+__device__ __forceinline__ uint32_t opaque(uint32_t v) {
+  asm volatile("" : "+v"(v));
+  return v;
+}
+
+// 8 codes (one dword) -> s * (q - 8) as fp16, in decode order.
+__device__ __forceinline__ half8v q4_decode(uint32_t w, half2v s2, uint32_t magic) {
   const half2v off = {(_Float16)-1032.0f, (_Float16)-1032.0f};
-  uint32_t d[4];
-  d[0] = (w & 0x000F000Fu) | 0x64006400u;
-  d[1] = ((w >> 8) & 0x000F000Fu) | 0x64006400u;
-  d[2] = ((w >> 4) & 0x000F000Fu) | 0x64006400u;
-  d[3] = ((w >> 12) & 0x000F000Fu) | 0x64006400u;
+  const half2v sixteenth = {(_Float16)0.0625f, (_Float16)0.0625f};
+  const half2v off16 = {(_Float16)-72.0f, (_Float16)-72.0f};
+  const uint32_t w8 = w >> 8;
+  const uint32_t d[4] = {(w & 0x000F000Fu) | magic, (w & 0x00F000F0u) | magic,
+                         (w8 & 0x000F000Fu) | magic, (w8 & 0x00F000F0u) | magic};
   half8v r;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     half2v h;
     __builtin_memcpy(&h, &d[i], 4);
-    h = (h + off) * s2;
+    // 1024 + q - 1032, or (1024 + 16 q) / 16 - 72: both exactly q - 8
+    h = (i & 1) ? __builtin_elementwise_fma(h, sixteenth, off16) : h + off;
+    h = h * s2;
     r[2 * i] = h[0];
     r[2 * i + 1] = h[1];
   }
@@ -76,8 +95,7 @@ struct StageQ {
 template <bool kPacked, int T, int R, int NM>
 __device__ __forceinline__ void load_q(StageQ<T, R, NM>& st, const u32x4* const* pc,
                                        const uint16_t* const* ps, const u32x4* const* xb,
-                                       int s, int hi) {
-  s = min(s, hi - 1);
+                                       int s) {
 #pragma unroll
   for (int m = 0; m < NM; ++m)
 #pragma unroll
@@ -93,13 +111,12 @@ __device__ __forceinline__ void load_q(StageQ<T, R, NM>& st, const u32x4* const*
 #pragma unroll
   for (int tt = 0; tt < T; ++tt)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) st.b[tt][j] = xb[tt][16 * s + j];
+    for (int j = 0; j < 4; ++j) st.b[tt][j] = xb[tt][16 * s + 4 * j];
 }
 
 template <int T, int R, int NM>
 __device__ __forceinline__ void compute_q(const StageQ<T, R, NM>& st, f32x4 (&acc)[NM][R][T],
-                                          int s, int hi) {
-  if (s >= hi) return;
+                                          uint32_t magic) {
 #pragma unroll
   for (int m = 0; m < NM; ++m)
 #pragma unroll
@@ -110,7 +127,7 @@ __device__ __forceinline__ void compute_q(const StageQ<T, R, NM>& st, f32x4 (&ac
       const half2v s2 = {sh, sh};
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const half8v a = q4_decode(st.c[m][r][j], s2);
+        const half8v a = q4_decode(st.c[m][r][j], s2, magic);
 #pragma unroll
         for (int tt = 0; tt < T; ++tt)
           acc[m][r][tt] = mfma16(a, as_half8(st.b[tt][j]), acc[m][r][tt]);
@@ -124,19 +141,19 @@ __device__ __forceinline__ void unit_pass_q(const FfnArgs& a, const Segment& seg
                                             const uint16_t* S0, const uint16_t* S1, f32x4* red) {
   constexpr int NM = kMode == 0 ? 2 : 1;
   const int lane = threadIdx.x & (kWave - 1);
-  const int wave = threadIdx.x >> 6;
+  const int wave = wave_id();
   const int rA = lane & 15, gK = lane >> 4;
   const int nss = K / 128;
   const int lo = wave * nss / W, hi = (wave + 1) * nss / W;
 
-  // fp16 activations in expansion order: x16 for gate-up, Hh for down.
+  // fp16 activations in decode order: x16 for gate-up, Hh for down.
   const uint16_t* X = static_cast<const uint16_t*>(kMode == 0 ? a.x16 : a.hh);
   const int ldx = kMode == 0 ? a.H : a.ldh;
   const u32x4* xb[T];
 #pragma unroll
   for (int tt = 0; tt < T; ++tt) {
     const int t = min(t0 + tt * 16 + rA, seg.n - 1);
-    xb[tt] = reinterpret_cast<const u32x4*>(X + (size_t)x_row(a, kMode, seg, t) * ldx) + 4 * gK;
+    xb[tt] = reinterpret_cast<const u32x4*>(X + (size_t)x_row(a, kMode, seg, t) * ldx) + gK;
   }
   const u32x4* pc[NM * R];
   const uint16_t* ps[NM * R];
@@ -169,15 +186,11 @@ __device__ __forceinline__ void unit_pass_q(const FfnArgs& a, const Segment& seg
 #pragma unroll
       for (int tt = 0; tt < T; ++tt) acc[m][r][tt] = f32x4{0.f, 0.f, 0.f, 0.f};
   if (hi > lo) {
-    StageQ<T, R, NM> st0, st1;
-    load_q<kPacked>(st0, pc, ps, xb, lo, hi);
-    for (int s = lo; s < hi; s += 2) {
-      if (s + 1 < hi) load_q<kPacked>(st1, pc, ps, xb, s + 1, hi);
-      compute_q(st0, acc, s, hi);
-      if (s + 1 >= hi) break;
-      if (s + 2 < hi) load_q<kPacked>(st0, pc, ps, xb, s + 2, hi);
-      compute_q(st1, acc, s + 1, hi);
-    }
+    const uint32_t magic = opaque(0x64006400u);
+    pipeline2<StageQ<T, R, NM>>(
+        hi - lo,
+        [&](StageQ<T, R, NM>& st, int i) { load_q<kPacked>(st, pc, ps, xb, lo + i); },
+        [&](const StageQ<T, R, NM>& st, int) { compute_q(st, acc, magic); });
   }
 
   if (W > 1) {
@@ -217,7 +230,8 @@ __device__ __forceinline__ void unit_pass_q(const FfnArgs& a, const Segment& seg
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
             const int f = r0 + 16 * r + 4 * gK + i;
-            dst[(f & ~7) + perm8(f & 7)] = (_Float16)(silu(acc[0][r][tt][i]) * acc[NM - 1][r][tt][i]);
+            dst[(block_pos(f >> 3) << 3) | pos8(f & 7)] =
+                (_Float16)(silu(acc[0][r][tt][i]) * acc[NM - 1][r][tt][i]);
           }
       } else {
         float* dst = a.out + (size_t)out_row(a, seg, t) * a.H;
@@ -268,7 +282,9 @@ __global__ __launch_bounds__(W * 64) void ffn_q4_kernel(FfnArgs a) {
   }
 }
 
-// x [B, H] bf16 -> x16 [B, H] fp16 in expansion order, one 8-block per thread.
+// x [B, H] bf16 -> x16 [B, H] fp16 in the kernels' order (block_pos, then
+// decode order inside each block), one 8-block per thread (H % 128 == 0, so
+// a row holds whole super-steps).
 __global__ __launch_bounds__(256) void q4_prep_x_kernel(const uint16_t* __restrict__ x,
                                                         uint16_t* __restrict__ x16, int n8) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
@@ -281,10 +297,10 @@ __global__ __launch_bounds__(256) void q4_prep_x_kernel(const uint16_t* __restri
     h[2 * q + 1] = (_Float16)bf16_to_f32(v[q] >> 16);
   }
 #pragma unroll
-  for (int e = 0; e < 8; ++e) o[perm8(e)] = h[e];
+  for (int e = 0; e < 8; ++e) o[pos8(e)] = h[e];
   u32x4 r;
   __builtin_memcpy(&r, o, 16);
-  reinterpret_cast<u32x4*>(x16)[i] = r;
+  reinterpret_cast<u32x4*>(x16)[block_pos(i)] = r;
 }
 
 #ifndef S2MOE_Q4_STEPS_PER_WAVE
@@ -320,6 +336,25 @@ hipError_t launch_q4_mode(const FfnArgs& a, hipStream_t s) {
                   : launch_q4_mode_p<kMode, TMAX, R, false>(a, s);
 }
 
+// Tile choices per batch size: (TMAX token tiles held at once, row tiles per
+// wave for gate-up, row tiles per wave for down).  Buckets larger than
+// 16 * TMAX tokens take several passes over the same weight rows.
+#ifndef S2MOE_Q4_SMALL
+#define S2MOE_Q4_SMALL 1, 2, 4
+#endif
+#ifndef S2MOE_Q4_MEDIUM
+#define S2MOE_Q4_MEDIUM 2, 1, 2
+#endif
+#ifndef S2MOE_Q4_LARGE
+#define S2MOE_Q4_LARGE 2, 2, 2
+#endif
+
+template <int TMAX, int RG, int RD>
+hipError_t launch_q4_pair(const FfnArgs& a, hipStream_t s) {
+  hipError_t err = launch_q4_mode<0, TMAX, RG>(a, s);
+  return err != hipSuccess ? err : launch_q4_mode<1, TMAX, RD>(a, s);
+}
+
 }  // namespace
 
 hipError_t launch_ffn_q4(const FfnArgs& a, hipStream_t s) {
@@ -328,16 +363,9 @@ hipError_t launch_ffn_q4(const FfnArgs& a, hipStream_t s) {
                      static_cast<const uint16_t*>(a.x), static_cast<uint16_t*>(a.x16), n8);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
-  if (a.B <= 16) {
-    err = launch_q4_mode<0, 1, 2>(a, s);
-    return err != hipSuccess ? err : launch_q4_mode<1, 1, 4>(a, s);
-  }
-  if (a.B <= 32) {
-    err = launch_q4_mode<0, 2, 1>(a, s);
-    return err != hipSuccess ? err : launch_q4_mode<1, 2, 2>(a, s);
-  }
-  err = launch_q4_mode<0, 4, 1>(a, s);
-  return err != hipSuccess ? err : launch_q4_mode<1, 4, 1>(a, s);
+  if (a.B <= 16) return launch_q4_pair<S2MOE_Q4_SMALL>(a, s);
+  if (a.B <= 32) return launch_q4_pair<S2MOE_Q4_MEDIUM>(a, s);
+  return launch_q4_pair<S2MOE_Q4_LARGE>(a, s);
 }
 
 }  // namespace s2moe

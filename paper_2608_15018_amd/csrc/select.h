@@ -25,12 +25,6 @@ __device__ __forceinline__ uint64_t lanemask_lt() {
   return lane == 0 ? 0ull : (~0ull >> (64 - lane));
 }
 
-// Index of the calling wave in its workgroup, as a wave-uniform value (so
-// that loops over it stay scalar).
-__device__ __forceinline__ int wave_id() {
-  return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-}
-
 // Wave-wide reductions through DPP lane moves (quad permutes, row mirrors,
 // row broadcasts), finished by reading lane 63.  The combination order is
 // fixed, so results are deterministic.  Lanes a move does not reach take
