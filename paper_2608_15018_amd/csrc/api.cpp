@@ -97,17 +97,27 @@ s2moe_status check_layer(const char* fn, const s2moe_layer* L, int32_t B) {
 size_t round256(size_t n) { return (n + 255) & ~(size_t)255; }
 
 // Workspace: the SwiGLU activations Hh [B*k + S*B, max(F, F_s)] (fp32 for
-// fp32 weights, else 16-bit), then for int4 weights an fp16 copy of x.
+// fp32 weights, else 16-bit); for int4 weights then an fp16 copy of x.
+size_t hh_rows(const s2moe_layer* L, int32_t B) {
+  return (size_t)B * L->top_k + (size_t)L->n_shared * B;
+}
+
+size_t hh_ld(const s2moe_layer* L) {
+  return (size_t)(L->n_shared > 0 && L->ffn_shared > L->ffn ? L->ffn_shared : L->ffn);
+}
+
 size_t hh_bytes(const s2moe_layer* L, int32_t B) {
-  const size_t rows = (size_t)B * L->top_k + (size_t)L->n_shared * B;
-  const size_t ldh = (size_t)(L->n_shared > 0 && L->ffn_shared > L->ffn ? L->ffn_shared : L->ffn);
   const size_t elt = L->w_dtype == S2MOE_F32 ? 4 : 2;
-  return round256(rows * ldh * elt);
+  return round256(hh_rows(L, B) * hh_ld(L) * elt);
+}
+
+size_t x16_bytes(const s2moe_layer* L, int32_t B) {
+  return round256((size_t)B * L->hidden * 2);
 }
 
 size_t workspace_bytes(const s2moe_layer* L, int32_t B) {
   size_t n = hh_bytes(L, B);
-  if (L->w_dtype == S2MOE_Q4G32) n += round256((size_t)B * L->hidden * 2);
+  if (L->w_dtype == S2MOE_Q4G32) n += x16_bytes(L, B);
   return n;
 }
 
@@ -278,10 +288,10 @@ s2moe_status s2moe_verify_moe(const s2moe_layer* layer, int32_t n_tokens, const 
   a.sh_gate_s = w->sh_gate_s;
   a.sh_up_s = w->sh_up_s;
   a.sh_down_s = w->sh_down_s;
-  a.hh = workspace;
-  a.x16 = q4 ? static_cast<char*>(workspace) + hh_bytes(layer, n_tokens) : nullptr;
-  a.ldh = (layer->n_shared > 0 && layer->ffn_shared > layer->ffn) ? layer->ffn_shared
-                                                                   : layer->ffn;
+  char* ws = static_cast<char*>(workspace);
+  a.hh = ws;
+  a.ldh = (int)hh_ld(layer);
+  a.x16 = q4 ? ws + hh_bytes(layer, n_tokens) : nullptr;
   a.out = expert_out;
   a.packed = (layer->flags & S2MOE_PACKED_WEIGHTS) != 0;
   return hip_status(fn, s2moe::launch_ffn(a, static_cast<hipStream_t>(stream)));

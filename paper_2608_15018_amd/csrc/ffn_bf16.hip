@@ -246,23 +246,33 @@ hipError_t launch_mode(const FfnArgs& a, hipStream_t s) {
                   : launch_mode_p<kMode, TMAX, R, U, false>(a, s);
 }
 
-}  // namespace
-
 // Token tiles held at once (TMAX) follow the batch size; larger buckets take
 // several passes over the same weight rows.  Row tiles per wave (R) grow
 // with TMAX so that activation reads from L2 stay below the weight stream.
+// Each choice is (TMAX, R gate-up, steps per stage gate-up, R down, steps
+// per stage down).
+#ifndef S2MOE_BF16_SMALL
+#define S2MOE_BF16_SMALL 1, 1, 2, 1, 4
+#endif
+#ifndef S2MOE_BF16_MEDIUM
+#define S2MOE_BF16_MEDIUM 2, 2, 2, 2, 2
+#endif
+#ifndef S2MOE_BF16_LARGE
+#define S2MOE_BF16_LARGE 4, 2, 1, 4, 1
+#endif
+
+template <int TMAX, int RG, int UG, int RD, int UD>
+hipError_t launch_bf16_pair(const FfnArgs& a, hipStream_t s) {
+  hipError_t err = launch_mode<0, TMAX, RG, UG>(a, s);
+  return err != hipSuccess ? err : launch_mode<1, TMAX, RD, UD>(a, s);
+}
+
+}  // namespace
+
 hipError_t launch_ffn_bf16(const FfnArgs& a, hipStream_t s) {
-  hipError_t err;
-  if (a.B <= 16) {
-    err = launch_mode<0, 1, 1, 2>(a, s);
-    return err != hipSuccess ? err : launch_mode<1, 1, 1, 4>(a, s);
-  }
-  if (a.B <= 32) {
-    err = launch_mode<0, 2, 2, 2>(a, s);
-    return err != hipSuccess ? err : launch_mode<1, 2, 2, 2>(a, s);
-  }
-  err = launch_mode<0, 4, 2, 1>(a, s);
-  return err != hipSuccess ? err : launch_mode<1, 4, 4, 1>(a, s);
+  if (a.B <= 16) return launch_bf16_pair<S2MOE_BF16_SMALL>(a, s);
+  if (a.B <= 32) return launch_bf16_pair<S2MOE_BF16_MEDIUM>(a, s);
+  return launch_bf16_pair<S2MOE_BF16_LARGE>(a, s);
 }
 
 }  // namespace s2moe

@@ -66,7 +66,7 @@ struct FfnArgs {
   const void *sh_gate_s, *sh_up_s, *sh_down_s;
   void* hh;  // workspace: SwiGLU activations [B*k + S*B, ldh] (fp32, bf16 or fp16)
   int ldh;
-  void* x16;  // workspace, int4 weights only: x as fp16 [B, H] in decode order
+  void* x16;  // workspace, int4 weights only: x as fp16 [B, H] in the kernels' order
   bool packed;  // weights in the packed tile order (pack.hip)
   float* out;  // [B*k + S*B, H]
 };
