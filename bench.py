@@ -9,8 +9,12 @@ enqueued back to back on one HIP stream with all inputs resident in HBM.
 Prints one JSON line.  `value` is draft tokens per second of whole steps;
 `roofline` covers the expert-FFN launches of s2moe_verify_moe (gate-up and
 down), timed with HIP events on the stream they run on, against the unique
-expert weight bytes the step must read; `cpu_baseline` times the fp64 oracle
-on the host for the same step.
+expert weight bytes the step must read; before each of those timed launches
+a 512 MiB write evicts the L2 caches and the 256 MB last-level cache, so no
+weight byte is served from cache.  `stream_read` is a plain read-only pass
+over 2 GiB on the same GPU (what the box delivers to a simple streaming
+read), and `cpu_baseline` times the fp64 oracle on the host for the same
+step.
 """
 
 from __future__ import annotations
@@ -52,12 +56,19 @@ FFN_SOURCES = {
 
 def ffn_source_hash(wdt: str) -> str:
     """sha256 of the sources the expert-FFN kernels of this weight format are
-    built from (identifies the kernel a traffic measurement belongs to)."""
+    built from (identifies the kernel a traffic measurement belongs to).  Of
+    kernels.h only the FfnArgs definition counts: the rest declares other
+    kernels."""
     import hashlib
+    import re
     h = hashlib.sha256()
     for f in FFN_SOURCES[wdt]:
         with open(os.path.join(ROOT, "paper_2608_15018_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
+            data = fh.read()
+        if f == "kernels.h":
+            m = re.search(rb"struct FfnArgs \{.*?\n\};", data, re.S)
+            data = m.group(0) if m else data
+        h.update(data)
     return h.hexdigest()
 
 
@@ -96,6 +107,8 @@ def main(argv=None):
                     help="stream the row-major weights instead of the packed tile order")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run a plain device copy of 1 GiB (calibrates HBM byte counters)")
+    ap.add_argument("--no-scrub", action="store_true",
+                    help="do not evict the caches before each timed expert-FFN launch")
     args = ap.parse_args(argv)
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -167,10 +180,13 @@ def main(argv=None):
     # stream around the expert-FFN launches of s2moe_verify_moe.
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
           for _ in range(args.steps)]
+    scrub = None if args.no_scrub else torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
     torch.cuda.synchronize()
     for i in range(args.steps):
         p.route(xd, rd)
         p.reuse_gate(cd)
+        if scrub is not None:
+            scrub.fill_(i & 0xFF)  # outside the events
         ev[i][0].record(stream)
         p.verify_moe(xd, wstruct)
         ev[i][1].record(stream)
@@ -179,7 +195,24 @@ def main(argv=None):
     ffn_ms = [a.elapsed_time(b) for a, b in ev]
     ffn_avg_s = float(np.mean(ffn_ms)) / 1e3
     achieved = unique_bytes / ffn_avg_s / 1e9
+    del scrub
 
+    # Reference: a plain sequential read of 2 GiB with the FFN's load type
+    # (s2moe_stream_read, a diagnostic of the library).
+    buf = torch.ones(1 << 29, dtype=torch.float32, device="cuda")
+    sink = torch.empty(s2.STREAM_SINK_WORDS, dtype=torch.int32, device="cuda")
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    s2.stream_read(buf, sink)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(5):
+        s2.stream_read(buf, sink)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    stream_gbs = 5 * buf.numel() * 4 / (e0.elapsed_time(e1) / 1e3) / 1e9
+    del buf, sink
+
+    scrub_note = None if args.no_scrub else "512 MiB write before each timed FFN launch"
     cpu = None
     if not args.no_cpu_baseline:
         import oracle
@@ -222,8 +255,12 @@ def main(argv=None):
         "cpu_baseline": cpu,
         "n_uniq": n_uniq,
         "reuse_ratio": n_uniq / (B * shape.top_k),
-        "ffn_us_p10_p90": [float(np.percentile(ffn_ms, 10)) * 1e3,
-                           float(np.percentile(ffn_ms, 90)) * 1e3],
+        "ffn_us_p10_p50_p90": [float(np.percentile(ffn_ms, q)) * 1e3 for q in (10, 50, 90)],
+        "cache_scrub": scrub_note,
+        "stream_read": {"value": stream_gbs, "unit": "GB/s",
+                        "kind": "s2moe_stream_read: one sequential pass over 2 GiB, 16-byte "
+                                "nontemporal loads",
+                        "ffn_frac_of_stream": achieved / stream_gbs},
     }
     print(json.dumps(out), flush=True)
     return 0

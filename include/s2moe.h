@@ -183,6 +183,18 @@ s2moe_status s2moe_combine(const s2moe_layer *layer, int32_t n_tokens,
                            const s2moe_routing *r, const float *expert_out, float *y,
                            void *stream);
 
+/* Diagnostic, not a step of the verify pass: read `bytes` of device memory
+   at `src` once, front to back, with the same 16-byte nontemporal loads the
+   expert-FFN kernels stream weights with, so that the rate a caller times
+   around it is what this GPU delivers to a plain sequential read.  `bytes`
+   must be a nonzero multiple of 16 and `src` 16-byte aligned.  `sink` is a
+   device buffer of S2MOE_STREAM_SINK_WORDS uint32; a prefix of it receives
+   one checksum word per block (the XOR of all words the block read, so the
+   XOR of that prefix is the XOR of the whole buffer).  Enqueued on
+   `stream`. */
+#define S2MOE_STREAM_SINK_WORDS 2048
+s2moe_status s2moe_stream_read(const void *src, size_t bytes, uint32_t *sink, void *stream);
+
 /* Message of the last failed call on this thread ("" if none). */
 const char *s2moe_last_error(void);
 

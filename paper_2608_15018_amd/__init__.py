@@ -14,6 +14,7 @@ from ._lib import (  # noqa: F401
     Q4G32,
     Layer,
     Routing,
+    STREAM_SINK_WORDS,
     S2moeError,
     Weights,
     abi_version,
@@ -24,6 +25,7 @@ from ._lib import (  # noqa: F401
     pack_weights,
     reuse_gate,
     route,
+    stream_read,
     verify_moe,
     workspace_bytes,
 )

@@ -82,6 +82,8 @@ def load():
     lib.s2moe_pack_weights.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
                                        ctypes.c_int32, P, P, P, P, P]
     lib.s2moe_pack_weights.restype = ctypes.c_int
+    lib.s2moe_stream_read.argtypes = [P, ctypes.c_size_t, P, P]
+    lib.s2moe_stream_read.restype = ctypes.c_int
     for f in ("s2moe_route", "s2moe_reuse_gate", "s2moe_verify_moe", "s2moe_combine"):
         getattr(lib, f).restype = ctypes.c_int
     lib.s2moe_last_error.restype = ctypes.c_char_p
@@ -240,6 +242,16 @@ def pack_weights(wdt: str, mats: torch.Tensor, scales: torch.Tensor | None = Non
     _check(load().s2moe_pack_weights(code, n, rows, cols, _ptr(mats), _ptr(scales), _ptr(dst),
                                      _ptr(dst_s), _stream(stream)))
     return dst, dst_s
+
+
+STREAM_SINK_WORDS = 2048
+
+
+def stream_read(buf: torch.Tensor, sink: torch.Tensor, stream=None):
+    """Diagnostic s2moe_stream_read: one sequential read of buf's bytes; sink
+    is a device tensor of at least STREAM_SINK_WORDS int32."""
+    _check(load().s2moe_stream_read(_ptr(buf), buf.numel() * buf.element_size(), _ptr(sink),
+                                    _stream(stream)))
 
 
 def abi_version() -> int:

@@ -297,6 +297,19 @@ s2moe_status s2moe_verify_moe(const s2moe_layer* layer, int32_t n_tokens, const 
   return hip_status(fn, s2moe::launch_ffn(a, static_cast<hipStream_t>(stream)));
 }
 
+s2moe_status s2moe_stream_read(const void* src, size_t bytes, uint32_t* sink, void* stream) {
+  const char* fn = "s2moe_stream_read";
+  if (src == nullptr || sink == nullptr) return fail(S2MOE_EINVAL, "%s: NULL pointer", fn);
+  if (!aligned16(src) || !aligned16(sink))
+    return fail(S2MOE_EINVAL, "%s: pointers must be 16-byte aligned", fn);
+  if (bytes == 0 || bytes % 16 != 0)
+    return fail(S2MOE_EINVAL, "%s: bytes = %zu, need a nonzero multiple of 16", fn, bytes);
+  // 2 waves per SIMD, each streaming one long contiguous range: the
+  // fastest plain read pattern measured on MI355X.
+  return hip_status(fn, s2moe::launch_stream_read(src, bytes, sink, 512,
+                                                  static_cast<hipStream_t>(stream)));
+}
+
 s2moe_status s2moe_pack_weights(int32_t w_dtype, int32_t n_mats, int32_t rows, int32_t cols,
                                 const void* src, const void* src_scales, void* dst,
                                 void* dst_scales, void* stream) {

@@ -88,6 +88,8 @@ struct PackArgs {
 };
 
 hipError_t launch_route(const RouteArgs& a, hipStream_t s);
+hipError_t launch_stream_read(const void* src, size_t bytes, uint32_t* sink, int blocks,
+                              hipStream_t s);
 hipError_t launch_pack(const PackArgs& a, hipStream_t s);
 hipError_t launch_reuse_gate(const GateArgs& a, hipStream_t s);
 hipError_t launch_ffn(const FfnArgs& a, hipStream_t s);

@@ -150,3 +150,13 @@ def test_pack_weights_rejects_overlap_and_missing_scales(lib):
 def test_packed_flag_needs_16bit_or_int4_weights(lib):
     st, msg = _route_status(lib, _layer(act="f32", wdt="f32", flags=8))
     assert st == _lib.EUNSUPPORTED and "PACKED" in msg
+
+
+def test_stream_read_validation(lib):
+    a = ctypes.c_void_p(0x100000)
+    assert lib.s2moe_stream_read(a, 0, a, None) == _lib.EINVAL
+    assert "multiple of 16" in _lib.last_error()
+    assert lib.s2moe_stream_read(a, 24, a, None) == _lib.EINVAL
+    assert lib.s2moe_stream_read(ctypes.c_void_p(0x100004), 64, a, None) == _lib.EINVAL
+    assert "aligned" in _lib.last_error()
+    assert lib.s2moe_stream_read(None, 64, a, None) == _lib.EINVAL

@@ -225,6 +225,21 @@ def test_near_ties_sharing_upper_key_bits(B, E, k, cap):
         assert np.abs(got["gate_w"] - ref["gate_w"]).max() <= TOL_GATE_W, label
 
 
+@pytest.mark.parametrize("nbytes", [16, 4096 + 48, (64 << 20) + 16 * 7])
+def test_stream_read_touches_every_byte_once(nbytes):
+    """The diagnostic read stream covers the buffer exactly once: the XOR of
+    its per-block checksum words equals the XOR of all 32-bit words."""
+    import paper_2608_15018_amd as s2
+    rng = np.random.default_rng(nbytes)
+    host = rng.integers(0, 1 << 32, size=nbytes // 4, dtype=np.uint32)
+    buf = torch.from_numpy(host.view(np.int32)).cuda()
+    sink = torch.zeros(s2.STREAM_SINK_WORDS, dtype=torch.int32, device="cuda")
+    s2.stream_read(buf, sink)
+    torch.cuda.synchronize()
+    got = np.bitwise_xor.reduce(sink.cpu().numpy().view(np.uint32))
+    assert got == np.bitwise_xor.reduce(host)
+
+
 # ---------------------------------------------------------------- packed weights
 def _expected_pack_bf16(m):
     """Reference tile order written out independently: tile (rt, s) of 16 rows
