@@ -207,29 +207,24 @@ __global__ __launch_bounds__(W * 64) void ffn_bf16_kernel(FfnArgs a) {
   }
 }
 
-#ifndef S2MOE_STEPS_PER_WAVE
-#define S2MOE_STEPS_PER_WAVE 16
-#endif
 #ifndef S2MOE_MAX_WAVES
 #define S2MOE_MAX_WAVES 8
 #endif
 
-// Waves per unit: enough that each streams >= S2MOE_STEPS_PER_WAVE K steps,
-// a power of two, and the reduction buffer stays within 32 KB of LDS.
-int pick_waves(int nks, int tiles) {
+// Waves per unit: enough that each streams >= spw K steps, a power of two,
+// and the reduction buffer stays within 32 KB of LDS.
+int pick_waves(int nks, int tiles, int spw) {
   int w = 1;
-  while (w * 2 <= S2MOE_MAX_WAVES && nks / (w * 2) >= S2MOE_STEPS_PER_WAVE &&
-         (w * 2) * tiles <= 32)
-    w *= 2;
+  while (w * 2 <= S2MOE_MAX_WAVES && nks / (w * 2) >= spw && (w * 2) * tiles <= 32) w *= 2;
   return w;
 }
 
 template <int kMode, int TMAX, int R, int U, bool kPacked>
-hipError_t launch_mode_p(const FfnArgs& a, hipStream_t s) {
+hipError_t launch_mode_p(const FfnArgs& a, int spw, hipStream_t s) {
   const int nm = kMode == 0 ? 2 : 1;
   int nks = kMode == 0 ? a.H / 32 : a.F / 32;
   if (kMode == 1 && a.S > 0) nks = min(nks, a.Fs / 32);
-  const int w = pick_waves(nks, nm * R * TMAX);
+  const int w = pick_waves(nks, nm * R * TMAX, spw);
   const dim3 grid(n_blocks(a, kMode, 16 * R));
   switch (w) {
     case 1: hipLaunchKernelGGL((ffn_bf16_kernel<kMode, TMAX, R, 1, U, kPacked>), grid, dim3(64), 0, s, a); break;
@@ -241,30 +236,30 @@ hipError_t launch_mode_p(const FfnArgs& a, hipStream_t s) {
 }
 
 template <int kMode, int TMAX, int R, int U>
-hipError_t launch_mode(const FfnArgs& a, hipStream_t s) {
-  return a.packed ? launch_mode_p<kMode, TMAX, R, U, true>(a, s)
-                  : launch_mode_p<kMode, TMAX, R, U, false>(a, s);
+hipError_t launch_mode(const FfnArgs& a, int spw, hipStream_t s) {
+  return a.packed ? launch_mode_p<kMode, TMAX, R, U, true>(a, spw, s)
+                  : launch_mode_p<kMode, TMAX, R, U, false>(a, spw, s);
 }
 
 // Token tiles held at once (TMAX) follow the batch size; larger buckets take
 // several passes over the same weight rows.  Row tiles per wave (R) grow
 // with TMAX so that activation reads from L2 stay below the weight stream.
 // Each choice is (TMAX, R gate-up, steps per stage gate-up, R down, steps
-// per stage down).
+// per stage down, minimum K steps per wave).
 #ifndef S2MOE_BF16_SMALL
-#define S2MOE_BF16_SMALL 1, 1, 2, 1, 4
+#define S2MOE_BF16_SMALL 1, 1, 2, 1, 4, 16
 #endif
 #ifndef S2MOE_BF16_MEDIUM
-#define S2MOE_BF16_MEDIUM 2, 2, 2, 2, 2
+#define S2MOE_BF16_MEDIUM 2, 2, 2, 2, 2, 32
 #endif
 #ifndef S2MOE_BF16_LARGE
-#define S2MOE_BF16_LARGE 4, 2, 1, 4, 1
+#define S2MOE_BF16_LARGE 4, 2, 1, 4, 1, 16
 #endif
 
-template <int TMAX, int RG, int UG, int RD, int UD>
+template <int TMAX, int RG, int UG, int RD, int UD, int SPW>
 hipError_t launch_bf16_pair(const FfnArgs& a, hipStream_t s) {
-  hipError_t err = launch_mode<0, TMAX, RG, UG>(a, s);
-  return err != hipSuccess ? err : launch_mode<1, TMAX, RD, UD>(a, s);
+  hipError_t err = launch_mode<0, TMAX, RG, UG>(a, SPW, s);
+  return err != hipSuccess ? err : launch_mode<1, TMAX, RD, UD>(a, SPW, s);
 }
 
 }  // namespace
