@@ -1,6 +1,6 @@
 """fp64 CPU oracle (test infrastructure; see s2moe_oracle)."""
 
-from . import s2moe_oracle  # noqa: F401
+from . import expand_oracle, s2moe_oracle  # noqa: F401
 from .s2moe_oracle import (  # noqa: F401
     BIAS_ABSOLUTE,
     GATE_FROM_BIASED,

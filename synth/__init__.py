@@ -1,4 +1,5 @@
-"""Seeded synthetic inputs for the verify-MoE pass.
+"""Seeded synthetic inputs for the verify-MoE pass and the draft-tree
+expansion that selects its tokens.
 
 This package only draws random numbers and stores them in the input formats
 (fp32, bf16 bit patterns, packed 4-bit codes with fp16 group scales).  It does
@@ -16,3 +17,4 @@ from .gen import (  # noqa: F401
     make_router,
     make_shared_experts,
 )
+from .trees import TREE_WORKLOADS, TreeWorkload, make_tree, make_trees  # noqa: F401

@@ -94,3 +94,28 @@ def test_margin_enforcement(name):
     assert m["cap_margin"] >= 1e-3
     for bm in m["biased"]:
         assert bm.min() >= 1e-3
+
+
+# ------------------------------------------------------------- draft trees
+def test_draft_trees_are_well_formed_and_seeded():
+    from synth.trees import TREE_WORKLOADS, make_trees
+    for wl in TREE_WORKLOADS.values():
+        d = make_trees(wl, 3, seed=5)
+        d2 = make_trees(wl, 3, seed=5)
+        for k in d:
+            np.testing.assert_array_equal(d[k], d2[k])
+        N = wl.max_nodes
+        assert d["parent"].shape == (3, N) and d["eid"].shape == (3, N, wl.n_layers, wl.k)
+        for t in range(3):
+            n = int(d["n_nodes"][t])
+            assert wl.branch + (wl.depth - 1) * wl.beam_min * wl.branch <= n <= N
+            par = d["parent"][t, :n]
+            assert (par < np.arange(n)).all() and (par >= -1).all()
+            q = d["q"][t, :n]
+            assert ((q >= 0) & (q <= 1)).all()
+            e = d["eid"][t, :n]
+            assert ((e >= 0) & (e < wl.n_experts)).all()
+            # k distinct experts per token and layer
+            s = np.sort(e, axis=-1)
+            assert (np.diff(s, axis=-1) > 0).all()
+            assert (d["eid"][t, n:] == -1).all()
