@@ -183,6 +183,73 @@ s2moe_status s2moe_combine(const s2moe_layer *layer, int32_t n_tokens,
                            const s2moe_routing *r, const float *expert_out, float *y,
                            void *stream);
 
+/* ---------------------------------------------------------------------------
+   Routing-aware adaptive speculative expansion (Sec. "Routing-aware Adaptive
+   Speculative Expansion"): which draft tokens enter the verify batch.
+
+   Each of T draft trees has up to N candidate tokens (nodes 0..n_t-1,
+   n_t = n_nodes[t]; a node's parent is an earlier node, or -1 for a child of
+   the root, the last verified token).  With
+     p_i   = q_i * p_parent(i)  (prefix confidence, "Expected Benefit"),
+     B_i   = p_i * T_AR,
+     dC_i  = |E_i \ U| * T_exp (Eq. of the marginal verification cost; E_i
+             the (layer, expert) pairs predicted for token i, U the union of
+             the pairs of the selected tokens, started from the root's),
+     U_i   = B_i / (dC_i + C_i^draft)  (Eq. of the utility),
+   the call repeatedly selects, among the unselected nodes whose parent is
+   selected (or is the root), the one of largest U_i (ties: smaller index),
+   while that U_i >= 1, up to max_admit selections.  Everything is computed
+   in fp64 as B / (n * T_exp + c) without fused multiply-adds, so results
+   are reproducible bit for bit.
+
+   A node is never selected, nor anything below it, if its parent is not -1
+   or an earlier node (status bit 1), its q is not in [0, 1] (bit 2) or its
+   C^draft is not finite and positive (bit 4); an n_nodes value outside
+   [0, N] is clamped (bit 8).  Expert ids outside [0, E) are padding and
+   repeated ids count once.
+
+   All arrays are device memory, padded per tree to N nodes, row-major:
+     parent   [T][N]       int32
+     q        [T][N]       float  draft confidence of node i given its prefix
+     eid      [T][N][L][k] int32  predicted experts per MoE layer
+     c_draft  [T][N]       float  C_i^draft
+     root_eid [T][L][k]    int32  experts of the root token, or NULL (U starts empty)
+     n_nodes  [T]          int32
+   and written:
+     order    [T][N]  int32   selected nodes in selection order, -1 after
+     util     [T][N]  double  U_i at each selection, 0 after
+     n_new    [T][N]  int32   |E_i \ U| at each selection, 0 after
+     n_admit  [T]     int32   number selected
+     n_pairs  [T]     int32   |U| at the end (root pairs included)
+     status   [T]     int32   bits above, 0 if every node was valid
+   Limits: 1 <= N <= 1024, 1 <= L <= 128, 1 <= E <= 1024, 1 <= k <= 32, and
+   the tree state (about L * E * ceil(N / 32) * 4 + 13 N bytes) must fit in
+   one workgroup's LDS (s2moe_expand_max_nodes); T_AR and T_exp finite and
+   >= 0.  Errors: S2MOE_EINVAL for a malformed argument, S2MOE_EUNSUPPORTED
+   when the tree state does not fit.  T = 0 is a no-op.  Enqueued on
+   `stream`; one workgroup per tree. */
+typedef struct s2moe_expand_shape {
+  int32_t n_trees;    /* T                                              */
+  int32_t max_nodes;  /* N: padded nodes per tree                       */
+  int32_t n_layers;   /* L: MoE layers whose experts are predicted      */
+  int32_t n_experts;  /* E                                              */
+  int32_t k;          /* ids per token and layer (-1 padding allowed)   */
+  int32_t max_admit;  /* selections per tree, <= 0: no limit           */
+  double t_ar;        /* T_AR: one target decoding step                 */
+  double t_exp;       /* T_exp: one more expert at one layer            */
+} s2moe_expand_shape;
+
+s2moe_status s2moe_expand(const s2moe_expand_shape *shape, const int32_t *parent,
+                          const float *q, const int32_t *eid, const float *c_draft,
+                          const int32_t *root_eid, const int32_t *n_nodes, int32_t *order,
+                          double *util, int32_t *n_new, int32_t *n_admit, int32_t *n_pairs,
+                          int32_t *status, void *stream);
+
+/* Largest N (<= 1024) that s2moe_expand accepts for L layers, E experts and
+   k ids per layer on the current device; 0 if none. */
+s2moe_status s2moe_expand_max_nodes(int32_t n_layers, int32_t n_experts, int32_t k,
+                                    int32_t *max_nodes);
+
 /* Diagnostic, not a step of the verify pass: read `bytes` of device memory
    at `src` once, front to back, with the same 16-byte nontemporal loads the
    expert-FFN kernels stream weights with, so that the rate a caller times

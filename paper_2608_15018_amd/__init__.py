@@ -1,4 +1,5 @@
-"""S2-MoE verify-MoE hot path for AMD Instinct MI355X (gfx950).
+"""S2-MoE verify-MoE hot path for AMD Instinct MI355X (gfx950), and the
+routing-aware draft-tree expansion that selects its tokens.
 
 The work happens in libs2moe.so (hand-written HIP, C ABI in include/s2moe.h);
 this package is its thin Python binding.
@@ -7,6 +8,7 @@ this package is its thin Python binding.
 from ._lib import (  # noqa: F401
     BF16,
     BIAS_ABSOLUTE,
+    ExpandOut,
     F32,
     GATE_FROM_BIASED,
     PACKED_WEIGHTS,
@@ -19,6 +21,8 @@ from ._lib import (  # noqa: F401
     Weights,
     abi_version,
     combine,
+    expand,
+    expand_max_nodes,
     load,
     make_layer,
     make_weights,

@@ -58,6 +58,13 @@ class RoutingStruct(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in _ROUTING_FIELDS]
 
 
+class ExpandShape(ctypes.Structure):
+    _fields_ = [("n_trees", ctypes.c_int32), ("max_nodes", ctypes.c_int32),
+                ("n_layers", ctypes.c_int32), ("n_experts", ctypes.c_int32),
+                ("k", ctypes.c_int32), ("max_admit", ctypes.c_int32),
+                ("t_ar", ctypes.c_double), ("t_exp", ctypes.c_double)]
+
+
 _lib = None
 
 
@@ -82,6 +89,11 @@ def load():
     lib.s2moe_pack_weights.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
                                        ctypes.c_int32, P, P, P, P, P]
     lib.s2moe_pack_weights.restype = ctypes.c_int
+    lib.s2moe_expand.argtypes = [ctypes.POINTER(ExpandShape)] + [P] * 13
+    lib.s2moe_expand.restype = ctypes.c_int
+    lib.s2moe_expand_max_nodes.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                                           ctypes.POINTER(ctypes.c_int32)]
+    lib.s2moe_expand_max_nodes.restype = ctypes.c_int
     lib.s2moe_stream_read.argtypes = [P, ctypes.c_size_t, P, P]
     lib.s2moe_stream_read.restype = ctypes.c_int
     for f in ("s2moe_route", "s2moe_reuse_gate", "s2moe_verify_moe", "s2moe_combine"):
@@ -242,6 +254,59 @@ def pack_weights(wdt: str, mats: torch.Tensor, scales: torch.Tensor | None = Non
     _check(load().s2moe_pack_weights(code, n, rows, cols, _ptr(mats), _ptr(scales), _ptr(dst),
                                      _ptr(dst_s), _stream(stream)))
     return dst, dst_s
+
+
+class ExpandOut:
+    """Device outputs of s2moe_expand for T trees of N nodes."""
+
+    def __init__(self, T: int, N: int, device="cuda"):
+        i32 = dict(dtype=torch.int32, device=device)
+        self.order = torch.empty((T, N), **i32)
+        self.util = torch.empty((T, N), dtype=torch.float64, device=device)
+        self.n_new = torch.empty((T, N), **i32)
+        self.n_admit = torch.empty(T, **i32)
+        self.n_pairs = torch.empty(T, **i32)
+        self.status = torch.empty(T, **i32)
+
+    def host(self) -> dict:
+        return {k: getattr(self, k).cpu().numpy()
+                for k in ("order", "util", "n_new", "n_admit", "n_pairs", "status")}
+
+
+def _expect(t, name, dtype, shape):
+    if t.dtype != dtype or tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name}: expected {dtype} {tuple(shape)}, got {t.dtype} {tuple(t.shape)}")
+
+
+def expand(parent, q, eid, c_draft, n_nodes, out: ExpandOut, n_experts: int, t_ar: float,
+           t_exp: float, root_eid=None, max_admit: int = 0, stream=None):
+    """s2moe_expand on device tensors: parent [T, N] int32, q [T, N] f32,
+    eid [T, N, L, k] int32, c_draft [T, N] f32, n_nodes [T] int32,
+    root_eid [T, L, k] int32 or None; results land in `out`."""
+    T, N, L, k = eid.shape
+    _expect(parent, "parent", torch.int32, (T, N))
+    _expect(q, "q", torch.float32, (T, N))
+    _expect(c_draft, "c_draft", torch.float32, (T, N))
+    _expect(n_nodes, "n_nodes", torch.int32, (T,))
+    _expect(eid, "eid", torch.int32, (T, N, L, k))
+    if root_eid is not None:
+        _expect(root_eid, "root_eid", torch.int32, (T, L, k))
+    for name in ("order", "n_new"):
+        _expect(getattr(out, name), name, torch.int32, (T, N))
+    _expect(out.util, "util", torch.float64, (T, N))
+    for name in ("n_admit", "n_pairs", "status"):
+        _expect(getattr(out, name), name, torch.int32, (T,))
+    sh = ExpandShape(T, N, L, n_experts, k, max_admit, t_ar, t_exp)
+    _check(load().s2moe_expand(ctypes.byref(sh), _ptr(parent), _ptr(q), _ptr(eid), _ptr(c_draft),
+                               _ptr(root_eid), _ptr(n_nodes), _ptr(out.order), _ptr(out.util),
+                               _ptr(out.n_new), _ptr(out.n_admit), _ptr(out.n_pairs),
+                               _ptr(out.status), _stream(stream)))
+
+
+def expand_max_nodes(n_layers: int, n_experts: int, k: int) -> int:
+    v = ctypes.c_int32(0)
+    _check(load().s2moe_expand_max_nodes(n_layers, n_experts, k, ctypes.byref(v)))
+    return int(v.value)
 
 
 STREAM_SINK_WORDS = 2048

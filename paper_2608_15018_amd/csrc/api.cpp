@@ -297,6 +297,117 @@ s2moe_status s2moe_verify_moe(const s2moe_layer* layer, int32_t n_tokens, const 
   return hip_status(fn, s2moe::launch_ffn(a, static_cast<hipStream_t>(stream)));
 }
 
+namespace {
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
+
+// LDS available to one workgroup on the current device.
+s2moe_status device_lds(const char* fn, size_t* bytes) {
+  int dev = 0, v = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e == hipSuccess) e = hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, dev);
+  if (e != hipSuccess) return fail(S2MOE_EHIP, "%s: %s", fn, hipGetErrorString(e));
+  *bytes = (size_t)v;
+  return S2MOE_OK;
+}
+
+s2moe_status check_expand_dims(const char* fn, int32_t L, int32_t E, int32_t k) {
+  if (L < 1 || L > 128) return fail(S2MOE_EINVAL, "%s: n_layers = %d not in [1, 128]", fn, L);
+  if (E < 1 || E > 1024) return fail(S2MOE_EINVAL, "%s: n_experts = %d not in [1, 1024]", fn, E);
+  if (k < 1 || k > 32) return fail(S2MOE_EINVAL, "%s: k = %d not in [1, 32]", fn, k);
+  return S2MOE_OK;
+}
+
+}  // namespace
+
+s2moe_status s2moe_expand_max_nodes(int32_t n_layers, int32_t n_experts, int32_t k,
+                                    int32_t* max_nodes) {
+  const char* fn = "s2moe_expand_max_nodes";
+  if (max_nodes == nullptr) return fail(S2MOE_EINVAL, "%s: max_nodes is NULL", fn);
+  *max_nodes = 0;
+  s2moe_status st = check_expand_dims(fn, n_layers, n_experts, k);
+  if (st != S2MOE_OK) return st;
+  size_t lds = 0;
+  if ((st = device_lds(fn, &lds)) != S2MOE_OK) return st;
+  int best = 0;
+  for (int n = 1; n <= 1024; ++n)
+    if (s2moe::expand_lds(n, n_layers, n_experts, k).total <= lds) best = n;
+  *max_nodes = best;
+  return ok();
+}
+
+s2moe_status s2moe_expand(const s2moe_expand_shape* shape, const int32_t* parent,
+                          const float* q, const int32_t* eid, const float* c_draft,
+                          const int32_t* root_eid, const int32_t* n_nodes, int32_t* order,
+                          double* util, int32_t* n_new, int32_t* n_admit, int32_t* n_pairs,
+                          int32_t* status, void* stream) {
+  const char* fn = "s2moe_expand";
+  if (shape == nullptr) return fail(S2MOE_EINVAL, "%s: shape is NULL", fn);
+  const s2moe_expand_shape& sh = *shape;
+  if (sh.n_trees < 0 || sh.n_trees > (1 << 24))
+    return fail(S2MOE_EINVAL, "%s: n_trees = %d not in [0, 2^24]", fn, sh.n_trees);
+  if (sh.max_nodes < 1 || sh.max_nodes > 1024)
+    return fail(S2MOE_EINVAL, "%s: max_nodes = %d not in [1, 1024]", fn, sh.max_nodes);
+  s2moe_status st = check_expand_dims(fn, sh.n_layers, sh.n_experts, sh.k);
+  if (st != S2MOE_OK) return st;
+  if (!std::isfinite(sh.t_ar) || sh.t_ar < 0.0 || !std::isfinite(sh.t_exp) || sh.t_exp < 0.0)
+    return fail(S2MOE_EINVAL, "%s: t_ar = %g, t_exp = %g must be finite and >= 0", fn, sh.t_ar,
+                sh.t_exp);
+  if (sh.n_trees == 0) return ok();
+  const struct {
+    const void* p;
+    size_t align;
+    const char* name;
+  } ptrs[] = {{parent, 4, "parent"}, {q, 4, "q"},           {eid, 4, "eid"},
+              {c_draft, 4, "c_draft"}, {n_nodes, 4, "n_nodes"}, {order, 4, "order"},
+              {util, 8, "util"},     {n_new, 4, "n_new"},   {n_admit, 4, "n_admit"},
+              {n_pairs, 4, "n_pairs"}, {status, 4, "status"}};
+  for (const auto& x : ptrs) {
+    if (x.p == nullptr) return fail(S2MOE_EINVAL, "%s: %s is NULL", fn, x.name);
+    if (!aligned(x.p, x.align))
+      return fail(S2MOE_EINVAL, "%s: %s is not %zu-byte aligned", fn, x.name, x.align);
+  }
+  if (root_eid != nullptr && !aligned(root_eid, 4))
+    return fail(S2MOE_EINVAL, "%s: root_eid is not 4-byte aligned", fn);
+  const size_t need = s2moe::expand_lds(sh.max_nodes, sh.n_layers, sh.n_experts, sh.k).total;
+  size_t lds = 0;
+  if ((st = device_lds(fn, &lds)) != S2MOE_OK) return st;
+  if (need > lds)
+    return fail(S2MOE_EUNSUPPORTED,
+                "%s: N = %d, L = %d, E = %d, k = %d needs %zu bytes of LDS per tree; the device "
+                "has %zu (s2moe_expand_max_nodes gives the largest N)",
+                fn, sh.max_nodes, sh.n_layers, sh.n_experts, sh.k, need, lds);
+  // l = j / k for j < L * k <= 4096 as one multiply and shift; checked here
+  // for every j the kernel will use.
+  const uint32_t magic = ((1u << 20) + (uint32_t)sh.k - 1) / (uint32_t)sh.k;
+  for (uint32_t j = 0; j < (uint32_t)(sh.n_layers * sh.k); ++j)
+    if (((j * magic) >> 20) != j / (uint32_t)sh.k)
+      return fail(S2MOE_EUNSUPPORTED, "%s: layer index shortcut fails for k = %d", fn, sh.k);
+  s2moe::ExpandArgs a{};
+  a.parent = parent;
+  a.q = q;
+  a.eid = eid;
+  a.c_draft = c_draft;
+  a.root_eid = root_eid;
+  a.n_nodes = n_nodes;
+  a.order = order;
+  a.util = util;
+  a.n_new = n_new;
+  a.n_admit = n_admit;
+  a.n_pairs = n_pairs;
+  a.status = status;
+  a.T = sh.n_trees;
+  a.N = sh.max_nodes;
+  a.L = sh.n_layers;
+  a.E = sh.n_experts;
+  a.k = sh.k;
+  a.max_admit = sh.max_admit;
+  a.k_magic = magic;
+  a.t_ar = sh.t_ar;
+  a.t_exp = sh.t_exp;
+  return hip_status(fn, s2moe::launch_expand(a, need, static_cast<hipStream_t>(stream)));
+}
+
 s2moe_status s2moe_stream_read(const void* src, size_t bytes, uint32_t* sink, void* stream) {
   const char* fn = "s2moe_stream_read";
   if (src == nullptr || sink == nullptr) return fail(S2MOE_EINVAL, "%s: NULL pointer", fn);

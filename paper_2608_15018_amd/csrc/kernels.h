@@ -87,6 +87,51 @@ struct PackArgs {
   bool q4;
 };
 
+// Routing-aware adaptive expansion over T padded draft trees of N nodes.
+struct ExpandArgs {
+  const int32_t* parent;    // [T][N]
+  const float* q;           // [T][N]
+  const int32_t* eid;       // [T][N][L][k]
+  const float* c_draft;     // [T][N]
+  const int32_t* root_eid;  // [T][L][k] or nullptr
+  const int32_t* n_nodes;   // [T]
+  int32_t* order;           // [T][N]
+  double* util;             // [T][N]
+  int32_t* n_new;           // [T][N]
+  int32_t* n_admit;         // [T]
+  int32_t* n_pairs;         // [T]
+  int32_t* status;          // [T]
+  int T, N, L, E, k, max_admit;
+  uint32_t k_magic;  // ceil(2^20 / k): j / k == (j * k_magic) >> 20 for j < L*k <= 4096
+  double t_ar, t_exp;
+};
+
+// Byte offsets of the expansion kernel's LDS regions; host and device use
+// the same function so the launch size and the carve-up agree.
+struct ExpandLds {
+  int nw;   // node words per (layer, expert) mask: ceil(N / 32)
+  int ew;   // expert words per layer in the union bitset: ceil(E / 32)
+  size_t mask, uni, cnt, ben, list, state, misc, total;
+};
+
+__host__ __device__ inline ExpandLds expand_lds(int N, int L, int E, int k) {
+  ExpandLds o;
+  o.nw = (N + 31) / 32;
+  o.ew = (E + 31) / 32;
+  size_t off = 0;
+  o.ben = off;    off += (size_t)N * 8;                          // p_i, then B_i (double)
+  o.mask = off;   off += (size_t)L * E * o.nw * 4;                // node masks per pair
+  o.uni = off;    off += (size_t)L * o.ew * 4;                    // union bitset
+  o.cnt = off;    off += (size_t)N * 4;                           // |E_i \ U| per node
+  o.list = off;   off += (size_t)2 * L * k * 4;                   // new pairs, two buffers
+  off = (off + 15) & ~(size_t)15;
+  o.misc = off;   off += 128;                                     // reductions and counters
+  o.state = off;  off += (size_t)N;                               // per-node flags
+  o.total = (off + 15) & ~(size_t)15;
+  return o;
+}
+
+hipError_t launch_expand(const ExpandArgs& a, size_t lds_bytes, hipStream_t s);
 hipError_t launch_route(const RouteArgs& a, hipStream_t s);
 hipError_t launch_stream_read(const void* src, size_t bytes, uint32_t* sink, int blocks,
                               hipStream_t s);

@@ -160,3 +160,47 @@ def test_stream_read_validation(lib):
     assert lib.s2moe_stream_read(ctypes.c_void_p(0x100004), 64, a, None) == _lib.EINVAL
     assert "aligned" in _lib.last_error()
     assert lib.s2moe_stream_read(None, 64, a, None) == _lib.EINVAL
+
+
+def _expand_call(lib, sh, ptr=0x100000, misalign=None):
+    args = [ctypes.c_void_p(ptr)] * 13
+    if misalign is not None:
+        args[misalign] = ctypes.c_void_p(ptr + 4)
+    return lib.s2moe_expand(ctypes.byref(sh) if sh is not None else None, *args)
+
+
+@pytest.mark.parametrize("field,value,needle", [
+    ("max_nodes", 0, "max_nodes"), ("max_nodes", 1025, "max_nodes"),
+    ("n_layers", 0, "n_layers"), ("n_layers", 129, "n_layers"),
+    ("n_experts", 0, "n_experts"), ("n_experts", 1025, "n_experts"),
+    ("k", 0, "k ="), ("k", 33, "k ="), ("n_trees", -1, "n_trees"),
+    ("t_ar", -1.0, "t_ar"), ("t_exp", float("nan"), "t_exp"), ("t_ar", float("inf"), "t_ar"),
+])
+def test_expand_rejects_bad_shapes_on_host(lib, field, value, needle):
+    sh = _lib.ExpandShape(4, 116, 48, 128, 8, 0, 512.0, 1.0)
+    setattr(sh, field, value)
+    assert _expand_call(lib, sh) == _lib.EINVAL
+    assert needle in _lib.last_error()
+
+
+def test_expand_null_misaligned_and_empty(lib):
+    assert _expand_call(lib, None) == _lib.EINVAL
+    sh = _lib.ExpandShape(0, 116, 48, 128, 8, 0, 512.0, 1.0)
+    assert _expand_call(lib, sh, ptr=0) == _lib.OK  # T = 0: no-op, pointers unused
+    sh.n_trees = 2
+    assert _expand_call(lib, sh, ptr=0) == _lib.EINVAL
+    assert "NULL" in _lib.last_error()
+    assert _expand_call(lib, sh, misalign=7) == _lib.EINVAL  # util must be 8-byte aligned
+    assert "util" in _lib.last_error() and "aligned" in _lib.last_error()
+    assert lib.s2moe_expand_max_nodes(48, 128, 8, None) == _lib.EINVAL
+    v = ctypes.c_int32(7)
+    assert lib.s2moe_expand_max_nodes(0, 128, 8, ctypes.byref(v)) == _lib.EINVAL and v.value == 0
+
+
+def test_expand_layer_index_shortcut_exhaustive():
+    """The kernel maps a flat id index j < L*k to its layer with
+    (j * ceil(2^20 / k)) >> 20; exact for every k <= 32 and j < 4096."""
+    for k in range(1, 33):
+        magic = ((1 << 20) + k - 1) // k
+        for j in range(4096):
+            assert (j * magic) >> 20 == j // k and j * magic < 2 ** 32
