@@ -93,12 +93,138 @@ def recorded_traffic(name: str, wdt: str):
         return None
 
 
+def expand_bytes(d: dict, L: int, k: int) -> int:
+    """Algorithmic HBM bytes of one s2moe_expand launch: each tree's node
+    records (parent, q, C^draft: 12 B) and predicted expert ids (L*k int32)
+    for its n_t nodes, the root's ids and n_nodes read once; order, util and
+    n_new (16 B per padded node) and the three per-tree counts written."""
+    T, N = d["parent"].shape
+    nodes = int(d["n_nodes"].sum())
+    return nodes * (12 + 4 * L * k) + T * (4 * L * k + 4) + T * N * 16 + T * 12
+
+
+def bench_expand(args) -> int:
+    """Routing-aware adaptive expansion: `--trees` draft trees of the named
+    model shape per s2moe_expand launch."""
+    import torch
+
+    import paper_2608_15018_amd as s2
+    from synth.trees import TREE_WORKLOADS, make_trees
+
+    wl = TREE_WORKLOADS[args.workload]
+    T = args.trees
+    t0 = time.time()
+    d = make_trees(wl, T, args.seed)
+    _log(f"[bench] {T} trees generated in {time.time() - t0:.1f}s")
+    dev = {k: torch.from_numpy(v).cuda() for k, v in d.items()}
+    N, L, k = wl.max_nodes, wl.n_layers, wl.k
+    out = s2.ExpandOut(T, N)
+    stream = torch.cuda.current_stream()
+
+    def launch(o=out, dd=dev):
+        s2.expand(dd["parent"], dd["q"], dd["eid"], dd["c_draft"], dd["n_nodes"], o,
+                  wl.n_experts, wl.t_ar, wl.t_exp, root_eid=dd["root_eid"])
+
+    for _ in range(max(1, args.warmup)):
+        launch()
+    torch.cuda.synchronize()
+    res = out.host()
+
+    # Timed: K launches, each after a 512 MiB write that evicts the inputs
+    # from L2 and the 256 MB Infinity Cache, HIP events around each launch on
+    # the launch stream.
+    scrub = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for i in range(args.steps):
+        scrub.fill_(i & 0xFF)
+        ev[i][0].record(stream)
+        launch()
+        ev[i][1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_start
+    ms = [a.elapsed_time(b) for a, b in ev]
+    avg_s = float(np.mean(ms)) / 1e3
+    nbytes = expand_bytes(d, L, k)
+    achieved = nbytes / avg_s / 1e9
+
+    # One tree per launch: the latency a single request sees.
+    one = {kk: v[:1].contiguous() for kk, v in dev.items()}
+    o1 = s2.ExpandOut(1, N)
+    for _ in range(3):
+        launch(o1, one)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(20):
+        launch(o1, one)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    one_us = e0.elapsed_time(e1) / 20 * 1e3
+    del scrub
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        from oracle import expand_oracle
+        t = time.perf_counter()
+        done = 0
+        while done < T and (done < 8 or time.perf_counter() - t < 10.0):
+            sl = slice(done, done + 1)
+            expand_oracle.expand(d["parent"][sl], d["q"][sl], d["eid"][sl], d["c_draft"][sl],
+                                 wl.n_experts, wl.t_ar, wl.t_exp, d["root_eid"][sl],
+                                 d["n_nodes"][sl])
+            done += 1
+        dt = time.perf_counter() - t
+        cpu = {"value": done / dt, "unit": "draft trees/s", "cores": 1, "kind": "oracle",
+               "sample": f"the first {done} trees of the batch, one at a time, pure Python "
+                         f"sets, {dt:.1f}s"}
+
+    line = {
+        "metric": "routing-aware expansion: draft trees/s (Eq. U greedy selection per tree)",
+        "value": T / avg_s,
+        "unit": "draft trees/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": avg_s * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int32 ids, fp64 utilities",
+        "data": "synthetic",
+        "config": {"workload": wl.description, "name": wl.name, "trees": T, "max_nodes": N,
+                   "layers": L, "experts": wl.n_experts, "k": k, "t_ar": wl.t_ar,
+                   "t_exp": wl.t_exp, "c_draft": wl.c_draft},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "kernel": "s2moe_expand", "bytes_per_launch": nbytes,
+                     "avg_launch_us": avg_s * 1e6},
+        "cpu_baseline": cpu,
+        "launch_us_p10_p50_p90": [float(np.percentile(ms, q)) * 1e3 for q in (10, 50, 90)],
+        "wall_ms_per_step_incl_scrub": wall / args.steps * 1e3,
+        "one_tree_us": one_us,
+        "mean_nodes": float(d["n_nodes"].mean()),
+        "mean_selected": float(res["n_admit"].mean()),
+        "mean_union_pairs": float(res["n_pairs"].mean()),
+        "cache_scrub": "512 MiB write before each timed launch",
+    }
+    print(json.dumps(line), flush=True)
+    return 0
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="c2", choices=["c1", "c2", "c3", "c4", "c5"])
+    ap.add_argument("--workload", default="c2",
+                    choices=["c1", "c2", "c3", "c4", "c5", "t_qwen3", "t_deepseek", "t_olmoe",
+                             "t_gptoss"],
+                    help="c*: verify-MoE layer; t_*: draft-tree expansion (s2moe_expand)")
+    ap.add_argument("--trees", type=int, default=256,
+                    help="t_* workloads: draft trees per s2moe_expand launch")
     ap.add_argument("--batch", type=int, default=None, help="draft tokens (default: workload's)")
     ap.add_argument("--alpha", type=float, default=None)
     ap.add_argument("--seed", type=int, default=1)
@@ -135,6 +261,8 @@ def main(argv=None):
                           "launches": 5}))
         return 0
     s2.load()
+    if args.workload.startswith("t_"):
+        return bench_expand(args)
     wl = WORKLOADS[args.workload]
     shape = wl.shape if args.alpha is None else wl.shape.with_(alpha=args.alpha)
     B = args.batch or wl.batches[-1 if args.workload == "c5" else 0]

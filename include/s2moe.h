@@ -211,7 +211,7 @@ s2moe_status s2moe_combine(const s2moe_layer *layer, int32_t n_tokens,
    All arrays are device memory, padded per tree to N nodes, row-major:
      parent   [T][N]       int32
      q        [T][N]       float  draft confidence of node i given its prefix
-     eid      [T][N][L][k] int32  predicted experts per MoE layer
+     eid      [T][N][L][k] int32  predicted experts per MoE layer (16-byte aligned)
      c_draft  [T][N]       float  C_i^draft
      root_eid [T][L][k]    int32  experts of the root token, or NULL (U starts empty)
      n_nodes  [T]          int32
@@ -223,8 +223,9 @@ s2moe_status s2moe_combine(const s2moe_layer *layer, int32_t n_tokens,
      n_pairs  [T]     int32   |U| at the end (root pairs included)
      status   [T]     int32   bits above, 0 if every node was valid
    Limits: 1 <= N <= 1024, 1 <= L <= 128, 1 <= E <= 1024, 1 <= k <= 32, and
-   the tree state (about L * E * ceil(N / 32) * 4 + 13 N bytes) must fit in
-   one workgroup's LDS (s2moe_expand_max_nodes); T_AR and T_exp finite and
+   the tree state (about (N + 1) * L * E' / 8 + 17 N bytes, E' = E rounded
+   up to a power of two >= 32) must fit in one
+   workgroup's LDS (s2moe_expand_max_nodes); T_AR and T_exp finite and
    >= 0.  Errors: S2MOE_EINVAL for a malformed argument, S2MOE_EUNSUPPORTED
    when the tree state does not fit.  T = 0 is a no-op.  Enqueued on
    `stream`; one workgroup per tree. */

@@ -369,6 +369,7 @@ s2moe_status s2moe_expand(const s2moe_expand_shape* shape, const int32_t* parent
   }
   if (root_eid != nullptr && !aligned(root_eid, 4))
     return fail(S2MOE_EINVAL, "%s: root_eid is not 4-byte aligned", fn);
+  if (!aligned(eid, 16)) return fail(S2MOE_EINVAL, "%s: eid is not 16-byte aligned", fn);
   const size_t need = s2moe::expand_lds(sh.max_nodes, sh.n_layers, sh.n_experts, sh.k).total;
   size_t lds = 0;
   if ((st = device_lds(fn, &lds)) != S2MOE_OK) return st;
@@ -377,12 +378,9 @@ s2moe_status s2moe_expand(const s2moe_expand_shape* shape, const int32_t* parent
                 "%s: N = %d, L = %d, E = %d, k = %d needs %zu bytes of LDS per tree; the device "
                 "has %zu (s2moe_expand_max_nodes gives the largest N)",
                 fn, sh.max_nodes, sh.n_layers, sh.n_experts, sh.k, need, lds);
-  // l = j / k for j < L * k <= 4096 as one multiply and shift; checked here
-  // for every j the kernel will use.
-  const uint32_t magic = ((1u << 20) + (uint32_t)sh.k - 1) / (uint32_t)sh.k;
-  for (uint32_t j = 0; j < (uint32_t)(sh.n_layers * sh.k); ++j)
-    if (((j * magic) >> 20) != j / (uint32_t)sh.k)
-      return fail(S2MOE_EUNSUPPORTED, "%s: layer index shortcut fails for k = %d", fn, sh.k);
+  // f / k for f < N L k <= 2^22 as one multiply and shift: the error of
+  // f * ceil(2^42 / k) / 2^42 is below f / 2^42 <= 2^-20 < 1 / k.
+  const uint64_t kdiv = ((1ull << 42) + (uint64_t)sh.k - 1) / (uint64_t)sh.k;
   s2moe::ExpandArgs a{};
   a.parent = parent;
   a.q = q;
@@ -402,7 +400,7 @@ s2moe_status s2moe_expand(const s2moe_expand_shape* shape, const int32_t* parent
   a.E = sh.n_experts;
   a.k = sh.k;
   a.max_admit = sh.max_admit;
-  a.k_magic = magic;
+  a.k_div = kdiv;
   a.t_ar = sh.t_ar;
   a.t_exp = sh.t_exp;
   return hip_status(fn, s2moe::launch_expand(a, need, static_cast<hipStream_t>(stream)));

@@ -2,19 +2,21 @@
 // Speculative Expansion"): best-first selection of draft-tree tokens by the
 // utility U_i = p_i T_AR / (|E_i \ U| T_exp + C_i^draft) while U_i >= 1.
 //
-// One workgroup of 256 threads per tree; the whole tree state lives in LDS:
-//   mask[(l*E + e) * nw + w]  bit i%32 of word w = i/32: node i predicts
-//                             expert e at layer l (an inverted index: which
-//                             nodes a (layer, expert) pair touches)
-//   uni[l * ew + e/32]        the union U of the selected tokens' pairs
-//   cnt[i]                    |E_i \ U|, kept current as U grows
-//   ben[i]                    p_i, then B_i = p_i T_AR
-// Phases: (1) clear, root experts into U, per-node validity; (2) one wave per
-// node streams its [L][k] ids once from HBM, sets its mask bits and counts
-// its distinct pairs outside U; (3) prefix confidences, resolved level by
-// level; (4) the greedy loop.  Each selection costs one scan of the pair
-// masks for the selected node's new pairs plus, per candidate, one mask test
-// per new pair -- no per-step pass over the ids.
+// One workgroup of 256 threads per tree; the tree's state lives in LDS as
+// expert bitsets of EW words (E rounded up to a power of two >= 32):
+//   rows[i][l][w]  the experts node i is predicted to use at layer l
+//   uni[l][w]      the union U of the selected tokens' (layer, expert) pairs
+//   ben[i]         p_i, then B_i = p_i T_AR;  cdr[i] = C_i^draft
+//   front[]        the current candidates (parent selected or the root)
+// so that repeated ids collapse by themselves, |E_i \ U| is
+// sum_l popcount(rows[i][l] & ~uni[l]) and U grows by a word-wise OR.
+// Phases: (1) per-node validity and the root's experts into U; (2) all
+// threads stream the tree's [n][L][k] ids from HBM once (16-byte loads, many
+// in flight) and set the row bits; (3) prefix confidences, resolved level by
+// level; (4) the greedy loop: each step lists the candidates, each 16-lane
+// row of each wave scores one candidate at a time (a lane per layer), the
+// block takes the largest U_i (ties: smaller index) and, if U_i >= 1, ORs
+// the node's rows into U.
 #include "common.h"
 #include "kernels.h"
 
@@ -28,11 +30,12 @@ constexpr uint8_t kValid = 1, kAdmitted = 2;
 struct Misc {
   double red_u[kWaves];
   int red_i[kWaves];
+  int red_n[kWaves];
   int counter[2];
+  int any[2];
   int status;
   int pairs;
 };
-
 static_assert(sizeof(Misc) <= 128, "Misc must fit its LDS slot");
 
 // U_i from the node's benefit, current new-pair count and C^draft, in the
@@ -48,22 +51,67 @@ __device__ __forceinline__ bool better(double u, int i, double bu, int bi) {
   return u > bu || (u == bu && i < bi);
 }
 
-template <int NPT>
+__device__ __forceinline__ int wave_sum_int(int v) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, kWave);
+  return v;
+}
+
+// Sum over each 16-lane row (DPP row shifts); the total lands in the row's
+// last lane.
+__device__ __forceinline__ int row16_sum(int v) {
+  v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xF, 0xF, false);  // row_shr:1
+  v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xF, 0xF, false);  // row_shr:2
+  v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xF, 0xF, false);  // row_shr:4
+  v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xF, 0xF, false);  // row_shr:8
+  return v;
+}
+
+__device__ __forceinline__ double readlane_f64(double v, int lane) {
+  const uint64_t u = __double_as_longlong(v);
+  const uint32_t lo = __builtin_amdgcn_readlane((int)(uint32_t)u, lane);
+  const uint32_t hi = __builtin_amdgcn_readlane((int)(uint32_t)(u >> 32), lane);
+  return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
+
+// popcount(a & ~b) over one EW-word bitset pair, read as aligned vectors.
+template <int EW>
+__device__ __forceinline__ int count_new(const uint32_t* a, const uint32_t* b) {
+  int c = 0;
+  if constexpr (EW == 1) {
+    c = __popc(a[0] & ~b[0]);
+  } else if constexpr (EW == 2) {
+    const uint64_t x = *reinterpret_cast<const uint64_t*>(a);
+    const uint64_t y = *reinterpret_cast<const uint64_t*>(b);
+    c = __popcll(x & ~y);
+  } else {
+#pragma unroll
+    for (int q = 0; q < EW / 4; ++q) {
+      const u32x4 x = reinterpret_cast<const u32x4*>(a)[q];
+      const u32x4 y = reinterpret_cast<const u32x4*>(b)[q];
+#pragma unroll
+      for (int w = 0; w < 4; ++w) c += __popc(x[w] & ~y[w]);
+    }
+  }
+  return c;
+}
+
+template <int NPT, int EW>
 __global__ __launch_bounds__(kThreads) void expand_kernel(ExpandArgs a) {
   extern __shared__ __align__(16) unsigned char lds[];
   const ExpandLds lay = expand_lds(a.N, a.L, a.E, a.k);
   double* ben = reinterpret_cast<double*>(lds + lay.ben);
-  uint32_t* mask = reinterpret_cast<uint32_t*>(lds + lay.mask);
+  uint32_t* rows = reinterpret_cast<uint32_t*>(lds + lay.rows);
   uint32_t* uni = reinterpret_cast<uint32_t*>(lds + lay.uni);
-  int* cnt = reinterpret_cast<int*>(lds + lay.cnt);
-  int* list = reinterpret_cast<int*>(lds + lay.list);
+  float* cdr = reinterpret_cast<float*>(lds + lay.cdr);
+  int* front = reinterpret_cast<int*>(lds + lay.front);
   Misc* misc = reinterpret_cast<Misc*>(lds + lay.misc);
   uint8_t* state = lds + lay.state;
 
   const int t = blockIdx.x;
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
-  const int L = a.L, E = a.E, k = a.k, N = a.N, nw = lay.nw, ew = lay.ew;
+  const int L = a.L, E = a.E, k = a.k, N = a.N;
   const int Lk = L * k;
   const size_t node0 = (size_t)t * N;
 
@@ -74,23 +122,14 @@ __global__ __launch_bounds__(kThreads) void expand_kernel(ExpandArgs a) {
     n = min(max(n, 0), N);
   }
 
-  // (1) clear the masks and the union; root experts; node validity.
-  const int mask_words = L * E * nw;
-  for (int w = tid; w < mask_words; w += kThreads) mask[w] = 0u;
-  for (int w = tid; w < L * ew; w += kThreads) uni[w] = 0u;
-  if (tid == 0) {
-    misc->counter[0] = 0;
-    misc->counter[1] = 0;
-    misc->status = 0;
-    misc->pairs = 0;
-  }
+  // (1) per-node records and the root's ids: one round of loads.
   int par[NPT];
-  double cdr[NPT];
+  double qd[NPT];
 #pragma unroll
   for (int m = 0; m < NPT; ++m) {
     const int i = tid + m * kThreads;
     par[m] = -1;
-    cdr[m] = 1.0;
+    qd[m] = 0.0;
     if (i < n) {
       const int pa = a.parent[node0 + i];
       const float qv = a.q[node0 + i];
@@ -100,46 +139,87 @@ __global__ __launch_bounds__(kThreads) void expand_kernel(ExpandArgs a) {
       if (!(qv >= 0.f && qv <= 1.f)) { ok = false; status |= 2; }
       if (!(cv > 0.f && cv < INFINITY)) { ok = false; status |= 4; }
       par[m] = pa;
-      cdr[m] = (double)cv;
+      qd[m] = (double)qv;
       state[i] = ok ? kValid : 0;
-      cnt[i] = 0;
+      cdr[i] = cv;
       // p_i is resolved (>= 0) once its parent's is; invalid nodes are
       // resolved at once with a value nothing reads.
       ben[i] = ok ? -1.0 : 0.0;
     }
   }
+  constexpr int kRootPer = 4096 / kThreads;  // L * k <= 4096
+  int rv[kRootPer];
+#pragma unroll
+  for (int r = 0; r < kRootPer; ++r) {
+    const int j = tid + r * kThreads;
+    rv[r] = -1;
+    if (a.root_eid != nullptr && j < Lk) rv[r] = a.root_eid[(size_t)t * Lk + j];
+  }
+  // Clear the n nodes' row bitsets (16-byte aligned, EW-word rows) and the
+  // union.
+  {
+    const int words = n * L * EW;
+    u32x4* r4 = reinterpret_cast<u32x4*>(rows);
+    for (int w = tid; w < (words >> 2); w += kThreads) r4[w] = u32x4{0u, 0u, 0u, 0u};
+    for (int w = (words & ~3) + tid; w < words; w += kThreads) rows[w] = 0u;
+    for (int w = tid; w < L * EW; w += kThreads) uni[w] = 0u;
+  }
+  if (tid == 0) {
+    misc->counter[0] = 0;
+    misc->counter[1] = 0;
+    misc->any[0] = 0;
+    misc->status = 0;
+    misc->pairs = 0;
+  }
   __syncthreads();
   if (status) atomicOr(&misc->status, status);
-  if (a.root_eid != nullptr) {
-    const int32_t* row = a.root_eid + (size_t)t * Lk;
-    for (int j = tid; j < Lk; j += kThreads) {
-      const int e = row[j];
-      const int l = (int)(((uint32_t)j * a.k_magic) >> 20);
-      if (e >= 0 && e < E) atomicOr(&uni[l * ew + (e >> 5)], 1u << (e & 31));
+#pragma unroll
+  for (int r = 0; r < kRootPer; ++r) {
+    const int j = tid + r * kThreads;
+    const int e = rv[r];
+    if (j < Lk && e >= 0 && e < E) {
+      const int l = (int)(((uint64_t)j * a.k_div) >> 42);
+      atomicOr(&uni[l * EW + (e >> 5)], 1u << (e & 31));
     }
   }
-  __syncthreads();
 
-  // (2) masks and initial counts: wave w takes nodes w, w + 4, ...; its lanes
-  // stream the node's contiguous [L][k] ids.
-  for (int i = wave_id(); i < n; i += kWaves) {
-    const int32_t* row = a.eid + (node0 + i) * (size_t)Lk;
-    const uint32_t bit = 1u << (i & 31);
-    uint32_t* col = mask + (i >> 5);
-    int fresh = 0;
-    for (int j = lane; j < Lk; j += kWave) {
-      const int e = __builtin_nontemporal_load(row + j);
-      if (e >= 0 && e < E) {
-        const int l = (int)(((uint32_t)j * a.k_magic) >> 20);
-        const int p = l * E + e;
-        const uint32_t old = atomicOr(&col[(size_t)p * nw], bit);
-        if (!(old & bit) && !((uni[l * ew + (e >> 5)] >> (e & 31)) & 1u)) ++fresh;
-      }
+  // (2) the tree's ids, one contiguous node-major run of n * L * k int32:
+  // id f belongs to row f / k (= node * L + layer); ids outside [0, E) are
+  // padding.
+  const size_t e0 = node0 * (size_t)Lk;
+  const int total = n * Lk;
+  const int32_t* src = a.eid + e0;
+  auto put = [&](int f, int e) {
+    if (e >= 0 && e < E) {
+      const int row = (int)(((uint64_t)f * a.k_div) >> 42);
+      atomicOr(&rows[row * EW + (e >> 5)], 1u << (e & 31));
+    }
+  };
+  // eid is 16-byte aligned, so the run's first 16-byte boundary is at
+  // element (4 - e0 mod 4) mod 4.
+  const int head = min(total, (int)((4u - (uint32_t)(e0 & 3u)) & 3u));
+  for (int f = tid; f < head; f += kThreads) put(f, src[f]);
+  const int nch = (total - head) >> 2;
+  const u32x4* body = reinterpret_cast<const u32x4*>(src + head);
+  constexpr int kBatch = 32;
+  for (int c0 = 0; c0 < nch; c0 += kThreads * kBatch) {
+    u32x4 v[kBatch];
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      const int c = c0 + tid + u * kThreads;
+      if (c < nch) v[u] = __builtin_nontemporal_load(body + c);
     }
 #pragma unroll
-    for (int s = 32; s >= 1; s >>= 1) fresh += __shfl_xor(fresh, s, kWave);
-    if (lane == 0) cnt[i] = fresh;
+    for (int u = 0; u < kBatch; ++u) {
+      const int c = c0 + tid + u * kThreads;
+      if (c < nch) {
+        const int f = head + 4 * c;
+#pragma unroll
+        for (int x = 0; x < 4; ++x) put(f + x, (int)v[u][x]);
+      }
+    }
   }
+  for (int f = head + 4 * nch + tid; f < total; f += kThreads) put(f, src[f]);
 
   // (3) prefix confidences, root-down: p_i = p_parent * q_i.  Each pass
   // reads resolved parents, then (after a barrier) writes, so no value is
@@ -152,10 +232,9 @@ __global__ __launch_bounds__(kThreads) void expand_kernel(ExpandArgs a) {
       const int i = tid + m * kThreads;
       nv[m] = -1.0;
       if (i < n && ben[i] < 0.0) {
-        const double qi = (double)a.q[node0 + i];
         const double pp = par[m] < 0 ? 1.0 : ben[par[m]];
         if (pp >= 0.0) {
-          nv[m] = pp * qi;
+          nv[m] = pp * qd[m];
           upd = 1;
         }
       }
@@ -164,95 +243,104 @@ __global__ __launch_bounds__(kThreads) void expand_kernel(ExpandArgs a) {
 #pragma unroll
     for (int m = 0; m < NPT; ++m)
       if (nv[m] >= 0.0) ben[tid + m * kThreads] = nv[m];
-    if (!__syncthreads_or(upd)) break;
+    // "any node resolved in this pass", double-buffered across passes
+    if (upd) misc->any[pass & 1] = 1;
+    if (tid == 0) misc->any[(pass + 1) & 1] = 0;
+    __syncthreads();
+    if (!misc->any[pass & 1]) break;
   }
-  double bv[NPT];
+  // B_i = p_i T_AR (each thread its own nodes; read by others after the
+  // first barrier of the loop).
 #pragma unroll
   for (int m = 0; m < NPT; ++m) {
     const int i = tid + m * kThreads;
-    bv[m] = i < n ? ben[i] * a.t_ar : 0.0;
+    if (i < n) ben[i] = ben[i] * a.t_ar;
   }
-  // masks, counts and ben are complete after the last pass's barrier.
 
   // (4) greedy selection.
+  const int sub = lane & 15;
   int s = 0;
   for (; s < n; ++s) {
     if (a.max_admit > 0 && s >= a.max_admit) break;
-    double bu = -1.0;
-    int bi = INT32_MAX;
+    // Candidates: valid, unselected, parent selected or the root.
+    int* ctr = &misc->counter[s & 1];
 #pragma unroll
     for (int m = 0; m < NPT; ++m) {
       const int i = tid + m * kThreads;
-      if (i < n && state[i] == kValid && (par[m] < 0 || (state[par[m]] & kAdmitted))) {
-        const double u = utility(bv[m], cnt[i], a.t_exp, cdr[m]);
+      if (i < n && state[i] == kValid && (par[m] < 0 || (state[par[m]] & kAdmitted)))
+        front[atomicAdd(ctr, 1)] = i;
+    }
+    __syncthreads();
+    const int nf = *ctr;
+    if (tid == 0) misc->counter[(s + 1) & 1] = 0;
+    // Each 16-lane row of each wave scores one candidate at a time; the
+    // row's last lane keeps the row's best.
+    double bu = -1.0;
+    int bi = INT32_MAX, bn = 0;
+    for (int x0 = wave_id() * 4; x0 < nf; x0 += kWaves * 4) {
+      const int x = x0 + (lane >> 4);
+      int c = 0, i = 0;
+      if (x < nf) {
+        i = front[x];
+        const uint32_t* ri = rows + (size_t)i * L * EW;
+        for (int l = sub; l < L; l += 16) c += count_new<EW>(ri + l * EW, uni + l * EW);
+      }
+      c = row16_sum(c);
+      if (x < nf && sub == 15) {
+        const double u = utility(ben[i], c, a.t_exp, (double)cdr[i]);
         if (better(u, i, bu, bi)) {
           bu = u;
           bi = i;
+          bn = c;
         }
       }
     }
+    // The wave's best of its four row leaders.
+    {
+      double wu = readlane_f64(bu, 15);
+      int wi = __builtin_amdgcn_readlane(bi, 15), wn = __builtin_amdgcn_readlane(bn, 15);
 #pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) {
-      const double ou = __shfl_xor(bu, off, kWave);
-      const int oi = __shfl_xor(bi, off, kWave);
-      if (better(ou, oi, bu, bi)) {
-        bu = ou;
-        bi = oi;
+      for (int g = 1; g < 4; ++g) {
+        const double gu = readlane_f64(bu, 16 * g + 15);
+        const int gi = __builtin_amdgcn_readlane(bi, 16 * g + 15);
+        if (better(gu, gi, wu, wi)) {
+          wu = gu;
+          wi = gi;
+          wn = __builtin_amdgcn_readlane(bn, 16 * g + 15);
+        }
       }
+      bu = wu;
+      bi = wi;
+      bn = wn;
     }
     if (lane == 0) {
       misc->red_u[wave_id()] = bu;
       misc->red_i[wave_id()] = bi;
+      misc->red_n[wave_id()] = bn;
     }
     __syncthreads();
     bu = misc->red_u[0];
     bi = misc->red_i[0];
+    bn = misc->red_n[0];
 #pragma unroll
     for (int w = 1; w < kWaves; ++w)
       if (better(misc->red_u[w], misc->red_i[w], bu, bi)) {
         bu = misc->red_u[w];
         bi = misc->red_i[w];
+        bn = misc->red_n[w];
       }
     if (bi == INT32_MAX || !(bu >= 1.0)) break;  // same decision in every thread
     const int j = bi;
-    int* lst = list + (s & 1) * Lk;
-    int* ctr = &misc->counter[s & 1];
     if (tid == 0) {
       state[j] |= kAdmitted;
       a.order[node0 + s] = j;
       a.util[node0 + s] = bu;
-      a.n_new[node0 + s] = cnt[j];
-      misc->counter[(s + 1) & 1] = 0;
+      a.n_new[node0 + s] = bn;
     }
-    // New pairs of j: its mask bits at pairs not yet in U.
-    const int jw = j >> 5;
-    const uint32_t jb = 1u << (j & 31);
-    for (int p = tid; p < L * E; p += kThreads) {
-      if (mask[(size_t)p * nw + jw] & jb) {
-        const int l = p / E;
-        const int e = p - l * E;
-        uint32_t* uw = &uni[l * ew + (e >> 5)];
-        const uint32_t ub = 1u << (e & 31);
-        if (!(*uw & ub)) {
-          atomicOr(uw, ub);
-          lst[atomicAdd(ctr, 1)] = p;
-        }
-      }
-    }
+    // U gains the selected node's rows (one word per thread).
+    const uint32_t* rj = rows + (size_t)j * L * EW;
+    for (int w = tid; w < L * EW; w += kThreads) uni[w] |= rj[w];
     __syncthreads();
-    // Each remaining node loses the new pairs it predicts.
-    const int na = *ctr;
-#pragma unroll
-    for (int m = 0; m < NPT; ++m) {
-      const int i = tid + m * kThreads;
-      if (i < n && !(state[i] & kAdmitted)) {
-        const uint32_t* col = mask + (i >> 5);
-        const int sh = i & 31;
-        int dec = 0;
-        for (int x = 0; x < na; ++x) dec += (col[(size_t)lst[x] * nw] >> sh) & 1u;
-        cnt[i] -= dec;
-      }
-    }
   }
 
   // Epilogue: padding of the per-selection outputs, union size, status.
@@ -262,9 +350,8 @@ __global__ __launch_bounds__(kThreads) void expand_kernel(ExpandArgs a) {
     a.n_new[node0 + x] = 0;
   }
   int pc = 0;
-  for (int w = tid; w < L * ew; w += kThreads) pc += __popc(uni[w]);
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) pc += __shfl_xor(pc, off, kWave);
+  for (int w = tid; w < L * EW; w += kThreads) pc += __popc(uni[w]);
+  pc = wave_sum_int(pc);
   if (lane == 0) atomicAdd(&misc->pairs, pc);
   __syncthreads();
   if (tid == 0) {
@@ -274,16 +361,29 @@ __global__ __launch_bounds__(kThreads) void expand_kernel(ExpandArgs a) {
   }
 }
 
-template <int NPT>
-hipError_t launch_npt(const ExpandArgs& a, size_t lds_bytes, hipStream_t s) {
+template <int NPT, int EW>
+hipError_t launch_ew(const ExpandArgs& a, size_t lds_bytes, hipStream_t s) {
   if (lds_bytes > 65536) {
-    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&expand_kernel<NPT>),
+    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&expand_kernel<NPT, EW>),
                                              hipFuncAttributeMaxDynamicSharedMemorySize,
                                              (int)lds_bytes);
     if (e != hipSuccess) return e;
   }
-  hipLaunchKernelGGL(expand_kernel<NPT>, dim3(a.T), dim3(kThreads), lds_bytes, s, a);
+  hipLaunchKernelGGL((expand_kernel<NPT, EW>), dim3(a.T), dim3(kThreads), lds_bytes, s, a);
   return hipGetLastError();
+}
+
+template <int NPT>
+hipError_t launch_npt(const ExpandArgs& a, size_t lds_bytes, hipStream_t s) {
+  switch (expand_words(a.E)) {
+    case 1: return launch_ew<NPT, 1>(a, lds_bytes, s);
+    case 2: return launch_ew<NPT, 2>(a, lds_bytes, s);
+    case 4: return launch_ew<NPT, 4>(a, lds_bytes, s);
+    case 8: return launch_ew<NPT, 8>(a, lds_bytes, s);
+    case 16: return launch_ew<NPT, 16>(a, lds_bytes, s);
+    case 32: return launch_ew<NPT, 32>(a, lds_bytes, s);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 }  // namespace

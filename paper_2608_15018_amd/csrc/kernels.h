@@ -102,31 +102,37 @@ struct ExpandArgs {
   int32_t* n_pairs;         // [T]
   int32_t* status;          // [T]
   int T, N, L, E, k, max_admit;
-  uint32_t k_magic;  // ceil(2^20 / k): j / k == (j * k_magic) >> 20 for j < L*k <= 4096
+  uint64_t k_div;  // ceil(2^42 / k): f / k == (f * k_div) >> 42 for f < 2^22, k <= 32
   double t_ar, t_exp;
 };
 
 // Byte offsets of the expansion kernel's LDS regions; host and device use
 // the same function so the launch size and the carve-up agree.
 struct ExpandLds {
-  int nw;   // node words per (layer, expert) mask: ceil(N / 32)
-  int ew;   // expert words per layer in the union bitset: ceil(E / 32)
-  size_t mask, uni, cnt, ben, list, state, misc, total;
+  int ew;  // words of one layer's expert bitset, ceil(E / 32) rounded up to a power of two
+  size_t ben, rows, uni, cdr, front, misc, state, total;
 };
 
+__host__ __device__ inline int expand_words(int E) {
+  int w = 1;
+  while (32 * w < E) w <<= 1;
+  return w;
+}
+
 __host__ __device__ inline ExpandLds expand_lds(int N, int L, int E, int k) {
+  (void)k;
   ExpandLds o;
-  o.nw = (N + 31) / 32;
-  o.ew = (E + 31) / 32;
+  o.ew = expand_words(E);
   size_t off = 0;
-  o.ben = off;    off += (size_t)N * 8;                          // p_i, then B_i (double)
-  o.mask = off;   off += (size_t)L * E * o.nw * 4;                // node masks per pair
-  o.uni = off;    off += (size_t)L * o.ew * 4;                    // union bitset
-  o.cnt = off;    off += (size_t)N * 4;                           // |E_i \ U| per node
-  o.list = off;   off += (size_t)2 * L * k * 4;                   // new pairs, two buffers
+  o.ben = off;    off += (size_t)N * 8;              // p_i, then B_i (double)
   off = (off + 15) & ~(size_t)15;
-  o.misc = off;   off += 128;                                     // reductions and counters
-  o.state = off;  off += (size_t)N;                               // per-node flags
+  o.rows = off;   off += (size_t)N * L * o.ew * 4;   // expert bitset per (node, layer)
+  o.uni = off;    off += (size_t)L * o.ew * 4;       // union bitset per layer
+  o.cdr = off;    off += (size_t)N * 4;              // C^draft
+  o.front = off;  off += (size_t)N * 4;              // candidate list
+  off = (off + 15) & ~(size_t)15;
+  o.misc = off;   off += 128;                        // reductions and counters
+  o.state = off;  off += (size_t)N;                  // per-node flags
   o.total = (off + 15) & ~(size_t)15;
   return o;
 }

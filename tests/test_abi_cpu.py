@@ -192,15 +192,19 @@ def test_expand_null_misaligned_and_empty(lib):
     assert "NULL" in _lib.last_error()
     assert _expand_call(lib, sh, misalign=7) == _lib.EINVAL  # util must be 8-byte aligned
     assert "util" in _lib.last_error() and "aligned" in _lib.last_error()
+    assert _expand_call(lib, sh, misalign=2) == _lib.EINVAL  # eid must be 16-byte aligned
+    assert "eid" in _lib.last_error()
     assert lib.s2moe_expand_max_nodes(48, 128, 8, None) == _lib.EINVAL
     v = ctypes.c_int32(7)
     assert lib.s2moe_expand_max_nodes(0, 128, 8, ctypes.byref(v)) == _lib.EINVAL and v.value == 0
 
 
-def test_expand_layer_index_shortcut_exhaustive():
-    """The kernel maps a flat id index j < L*k to its layer with
-    (j * ceil(2^20 / k)) >> 20; exact for every k <= 32 and j < 4096."""
+def test_expand_row_index_shortcut_exhaustive():
+    """The kernel maps a flat id index f < N*L*k <= 2^22 to its (node, layer)
+    row with (f * ceil(2^42 / k)) >> 42; exact for every k <= 32 and f."""
+    import numpy as np
+    f = np.arange(1 << 22, dtype=np.uint64)
     for k in range(1, 33):
-        magic = ((1 << 20) + k - 1) // k
-        for j in range(4096):
-            assert (j * magic) >> 20 == j // k and j * magic < 2 ** 32
+        magic = np.uint64(((1 << 42) + k - 1) // k)
+        assert ((f * magic) >> np.uint64(42) == f // np.uint64(k)).all(), k
+        assert int(magic) * ((1 << 22) - 1) < 2 ** 64
