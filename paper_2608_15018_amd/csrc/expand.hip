@@ -189,18 +189,21 @@ __global__ __launch_bounds__(kThreads) void expand_kernel(ExpandArgs a) {
   const size_t e0 = node0 * (size_t)Lk;
   const int total = n * Lk;
   const int32_t* src = a.eid + e0;
-  auto put = [&](int f, int e) {
-    if (e >= 0 && e < E) {
-      const int row = (int)(((uint64_t)f * a.k_div) >> 42);
-      atomicOr(&rows[row * EW + (e >> 5)], 1u << (e & 31));
-    }
+  // Sets bit e of the row's bitset; padding ORs 0 into word 0 (no branch).
+  auto set_bit = [&](uint32_t row, int e) {
+    const bool ok = (uint32_t)e < (uint32_t)E;
+    const uint32_t w = ok ? row * EW + ((uint32_t)e >> 5) : 0u;
+    atomicOr(&rows[w], ok ? 1u << (e & 31) : 0u);
   };
+  auto row_of = [&](uint32_t f) { return (uint32_t)(((uint64_t)f * a.k_div) >> 42); };
   // eid is 16-byte aligned, so the run's first 16-byte boundary is at
   // element (4 - e0 mod 4) mod 4.
   const int head = min(total, (int)((4u - (uint32_t)(e0 & 3u)) & 3u));
-  for (int f = tid; f < head; f += kThreads) put(f, src[f]);
+  for (int f = tid; f < head; f += kThreads) set_bit(row_of(f), src[f]);
   const int nch = (total - head) >> 2;
   const u32x4* body = reinterpret_cast<const u32x4*>(src + head);
+  // With head == 0 and k a multiple of 4, the four ids of a chunk share a row.
+  const bool same_row = head == 0 && (k & 3) == 0;
   constexpr int kBatch = 32;
   for (int c0 = 0; c0 < nch; c0 += kThreads * kBatch) {
     u32x4 v[kBatch];
@@ -213,13 +216,26 @@ __global__ __launch_bounds__(kThreads) void expand_kernel(ExpandArgs a) {
     for (int u = 0; u < kBatch; ++u) {
       const int c = c0 + tid + u * kThreads;
       if (c < nch) {
-        const int f = head + 4 * c;
+        const uint32_t f = head + 4 * c;
+        uint32_t row = row_of(f);
+        if (same_row) {
 #pragma unroll
-        for (int x = 0; x < 4; ++x) put(f + x, (int)v[u][x]);
+          for (int x = 0; x < 4; ++x) set_bit(row, (int)v[u][x]);
+        } else {
+          uint32_t pos = f - row * k;  // position of the first id in its row
+#pragma unroll
+          for (int x = 0; x < 4; ++x) {
+            set_bit(row, (int)v[u][x]);
+            if (++pos == (uint32_t)k) {
+              pos = 0;
+              ++row;
+            }
+          }
+        }
       }
     }
   }
-  for (int f = head + 4 * nch + tid; f < total; f += kThreads) put(f, src[f]);
+  for (int f = head + 4 * nch + tid; f < total; f += kThreads) set_bit(row_of(f), src[f]);
 
   // (3) prefix confidences, root-down: p_i = p_parent * q_i.  Each pass
   // reads resolved parents, then (after a barrier) writes, so no value is
