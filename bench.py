@@ -75,6 +75,49 @@ def ffn_source_hash(wdt: str) -> str:
     return h.hexdigest()
 
 
+def expand_source_hash() -> str:
+    """sha256 of expand.hip, common.h and the ExpandArgs / expand layout
+    definitions of kernels.h (the sources of the s2moe_expand kernel)."""
+    import hashlib
+    import re
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2608_15018_amd", "csrc")
+    for f in ("expand.hip", "common.h"):
+        with open(os.path.join(csrc, f), "rb") as fh:
+            h.update(fh.read())
+    with open(os.path.join(csrc, "kernels.h"), "rb") as fh:
+        data = fh.read()
+    for pat in (rb"struct ExpandArgs \{.*?\n\};", rb"struct ExpandLds \{.*?(?=hipError_t launch_expand)"):
+        m = re.search(pat, data, re.S)
+        h.update(m.group(0) if m else data)
+    return h.hexdigest()
+
+
+def _traffic_record(path: str, src_hash: str):
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    with open(path) as f:
+        for line in f:
+            key, _, v = line.strip().lstrip("- ").partition(":")
+            if key in ("traffic_bytes_per_launch", "kernel_source_sha256"):
+                vals[key] = v.strip().strip("`")
+    if vals.get("kernel_source_sha256") != src_hash:
+        return None
+    try:
+        return int(vals["traffic_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def recorded_expand_traffic(name: str, trees: int):
+    """HBM bytes per s2moe_expand launch of `trees` trees of this workload
+    from the committed rocprofv3 counter summary, or None if there is none
+    or the kernel changed since it was taken."""
+    return _traffic_record(os.path.join(ROOT, "profiles", f"expand_{name}_{trees}_traffic.md"),
+                           expand_source_hash())
+
+
 def recorded_traffic(name: str, wdt: str):
     """HBM bytes per s2moe_verify_moe call from the committed rocprofv3 counter
     summary of this workload, or None if there is none or the kernel sources
@@ -211,7 +254,8 @@ def bench_expand(args) -> int:
                    "layers": L, "experts": wl.n_experts, "k": k, "t_ar": wl.t_ar,
                    "t_exp": wl.t_exp, "c_draft": wl.c_draft},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": recorded_expand_traffic(wl.name, T),
                      "kernel": "s2moe_expand", "bytes_per_launch": nbytes,
                      "avg_launch_us": avg_s * 1e6},
         "cpu_baseline": cpu,
