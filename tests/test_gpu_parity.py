@@ -350,25 +350,23 @@ def test_full_c4_shared_routed():
     _full_check(wl.shape, d, "c4 full")
 
 
-def test_full_c5_int4_layers():
-    """Mixtral-shaped int4 layers at draft sizes 1, 4, 16, 64 (layer 0) and
-    16 (layer 23).  The oracle uses the exact fp32 values of the dequantised
-    weights (s * (q - 8) has at most 15 significant bits)."""
+@pytest.mark.parametrize("layer", [0, 11, 23])
+def test_full_c5_int4_layers(layer):
+    """Mixtral-shaped int4 layers 0, 11 and 23 of the 24-layer stack, each at
+    draft sizes 1, 4, 16 and 64.  The oracle uses the exact fp32 values of
+    the dequantised weights (s * (q - 8) has at most 15 significant bits)."""
     wl = WORKLOADS["c5"]
     sh = wl.shape
-    cases = [(0, 1), (0, 4), (0, 16), (0, 64), (23, 16)]
-    cache = {}
-    for layer, B in cases:
+    dw = deq = None
+    for B in (1, 4, 16, 64):
         d = _workload_inputs("c5", B, seed=1, layer=layer)
-        if layer not in cache:
-            cache.clear()
+        if dw is None:
             from paper_2608_15018_amd.pipeline import weights_to_device
             ex = d["experts"]
             deq = {n: np.stack([oracle.dequant_q4g32(ex[n][e], ex[n + "_s"][e]).astype(np.float32)
                                 for e in range(sh.n_experts)])
                    for n in ("gate", "up", "down")}
-            cache[layer] = (weights_to_device(ex, {}), deq)
-        dw, deq = cache[layer]
+            dw = weights_to_device(ex, {})
         log(f"[parity] c5 layer={layer} B={B}")
         got, _ = run_gpu(sh, d, dw)
         if B == 16:
