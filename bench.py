@@ -271,6 +271,131 @@ def bench_expand(args) -> int:
     return 0
 
 
+def bench_draft(args) -> int:
+    """Expert-sparse draft step: every MoE layer of the model at k_draft
+    experts per token, B = --batch tokens, eager and replayed from a HIP
+    graph.  The layers cycle through 8 distinct weight sets drawn on the
+    device (each set is far larger than the caches), and each layer has its
+    own hidden states and router."""
+    import torch
+
+    import paper_2608_15018_amd as s2
+    from paper_2608_15018_amd import draft
+    from synth import device_gen
+
+    name = args.workload[2:]
+    m = draft.DRAFT_MODELS[name]
+    B, wdt, L = args.batch or 1, args.wdt, m["layers"]
+    H, F, E, k = m["hidden"], m["ffn"], m["n_experts"], m["k_draft"]
+    S, Fs = m.get("n_shared", 0), m.get("ffn_shared", 0)
+    layer = draft.draft_layer(name, wdt)
+    n_sets = min(L, 8)
+    t0 = time.time()
+    sets = []
+    for j in range(n_sets):
+        ex = device_gen.expert_weights(E, F, H, wdt, args.seed, j)
+        sh = device_gen.expert_weights(S, Fs, H, wdt, args.seed, j, tag=1) if S else {}
+        dev, w = s2.pack_expert_weights((ex, sh), wdt)
+        del ex, sh
+        sets.append((dev, w))
+    inputs = [(device_gen.activations(B, H, args.seed, l, rho=0.3),
+               device_gen.router(E, H, args.seed, l), sets[l % n_sets][1]) for l in range(L)]
+    torch.cuda.synchronize()
+    _log(f"[bench] draft {name}: {n_sets} weight sets, {L} layers in {time.time() - t0:.1f}s")
+    step = draft.DraftStep(layer, B, inputs)
+    for _ in range(max(1, args.warmup)):
+        step()
+    torch.cuda.synchronize()
+    n_uniq = [int(p.rt.n_uniq.item()) for p in step.passes]
+    e_bytes = expert_bytes(layer_shape_of(m, wdt), F)
+    s_bytes = expert_bytes(layer_shape_of(m, wdt), Fs) if S else 0
+    nbytes = sum(n_uniq) * e_bytes + L * S * s_bytes
+
+    stream = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    _head_start()
+    e0.record(stream)
+    for _ in range(args.steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    eager_s = e0.elapsed_time(e1) / 1e3 / args.steps
+    step.capture()
+    step.replay()
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(args.steps):
+        step.replay()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    graph_s = e0.elapsed_time(e1) / 1e3 / args.steps
+    achieved = nbytes / graph_s / 1e9
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+        from synth.configs import LayerShape
+        bits = lambda t: t.view(torch.int16).cpu().numpy().view(np.uint16)  # noqa: E731
+        shape = LayerShape(hidden=H, ffn=F, n_experts=E, top_k=k, cap=k, alpha=0.0, n_shared=S,
+                           ffn_shared=Fs, act="bf16", wdt="bf16")
+        if wdt == "bf16":
+            x, router, _ = inputs[0]
+            p0 = step.passes[0]
+            used = p0.rt.uniq[: n_uniq[0]]
+            dev = sets[0][0]
+            ex_raw = device_gen.expert_weights(E, F, H, wdt, args.seed, 0)
+            experts = {n: np.zeros((E,) + tuple(v.shape[1:]), np.uint16) for n, v in ex_raw.items()}
+            for n, v in ex_raw.items():
+                experts[n][used.cpu().numpy()] = bits(v[used.long()])
+            del ex_raw
+            shared = {n: bits(v) for n, v in (device_gen.expert_weights(
+                S, Fs, H, wdt, args.seed, 0, tag=1).items() if S else [])}
+            t = time.perf_counter()
+            oracle.forward(bits(x), bits(router), np.ones(B, np.float32), experts, shared, shape)
+            dt = time.perf_counter() - t
+            cpu = {"value": B / (dt * L), "unit": "draft tokens/s", "cores": os.cpu_count(),
+                   "kind": "oracle", "sample": f"layer 0 of the step in fp64 numpy ({dt:.2f}s), "
+                                              f"scaled to {L} layers"}
+
+    line = {
+        "metric": "expert-sparse draft step: draft tokens/s over all MoE layers",
+        "value": B / graph_s,
+        "unit": "draft tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": graph_s * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": {"bf16": "bf16", "q4g32": "int4-g32/bf16"}[wdt],
+        "data": "synthetic",
+        "config": {"workload": f"{name}-shaped draft step: {L} MoE layers, H {H}, F {F}, "
+                               f"{E} experts, k_draft {k}" + (f", {S} shared" if S else ""),
+                   "name": args.workload, "draft_tokens": B, "layers": L, "k_draft": k,
+                   "weights": wdt, "weight_sets": n_sets},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "kernel": "draft step (route, gate, experts, combine per layer; HIP graph)",
+                     "bytes_per_launch": nbytes, "avg_launch_us": graph_s * 1e6},
+        "cpu_baseline": cpu,
+        "eager_ms_per_step": eager_s * 1e3,
+        "graph_speedup": eager_s / graph_s,
+        "experts_per_step": sum(n_uniq),
+    }
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+def layer_shape_of(m: dict, wdt: str):
+    from synth.configs import LayerShape
+    return LayerShape(hidden=m["hidden"], ffn=m["ffn"], n_experts=m["n_experts"],
+                      top_k=m["k_draft"], cap=m["k_draft"], alpha=0.0,
+                      n_shared=m.get("n_shared", 0), ffn_shared=m.get("ffn_shared", 0),
+                      act="bf16", wdt=wdt)
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -278,8 +403,11 @@ def main(argv=None):
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="c2",
                     choices=["c1", "c2", "c3", "c4", "c5", "t_qwen3", "t_deepseek", "t_olmoe",
-                             "t_gptoss"],
-                    help="c*: verify-MoE layer; t_*: draft-tree expansion (s2moe_expand)")
+                             "t_gptoss", "d_olmoe", "d_deepseek", "d_qwen3", "d_gptoss"],
+                    help="c*: verify-MoE layer; t_*: draft-tree expansion (s2moe_expand); "
+                         "d_*: expert-sparse draft step over a model's MoE layers")
+    ap.add_argument("--wdt", default="bf16", choices=["bf16", "q4g32"],
+                    help="d_* workloads: expert weight format")
     ap.add_argument("--trees", type=int, default=256,
                     help="t_* workloads: draft trees per s2moe_expand launch")
     ap.add_argument("--batch", type=int, default=None, help="draft tokens (default: workload's)")
@@ -321,6 +449,8 @@ def main(argv=None):
     s2.load()
     if args.workload.startswith("t_"):
         return bench_expand(args)
+    if args.workload.startswith("d_"):
+        return bench_draft(args)
     wl = WORKLOADS[args.workload]
     shape = wl.shape if args.alpha is None else wl.shape.with_(alpha=args.alpha)
     B = args.batch or wl.batches[-1 if args.workload == "c5" else 0]
