@@ -35,7 +35,7 @@ __device__ __forceinline__ bool resolve_block(const FfnArgs& a, int mode, int ro
   bid -= a.S * nbs;
   const int u = bid / nbr;
   *rb = bid % nbr;
-  if (u >= min(*a.n_uniq, a.E)) return false;
+  if (u >= min(*a.n_uniq, min(a.E, a.B * a.k))) return false;
   // The routing arrays come from the gating step; values outside their
   // ranges (routing never computed) make the block idle instead of faulting.
   const int e = a.uniq[u];
@@ -115,11 +115,15 @@ __device__ __forceinline__ void pipeline2(int n, Load&& load, Use&& use) {
   }
 }
 
-// Number of blocks of `rows_per_block` rows over all experts a launch covers.
+// Number of blocks of `rows_per_block` rows a launch covers: the shared
+// experts, then one slot per possibly activated expert.  A batch activates
+// at most min(E, B k) routed experts, so small batches (a draft step) do not
+// launch blocks for experts that cannot be in uniq.
 inline int n_blocks(const FfnArgs& a, int mode, int rows_per_block) {
   const int rows_r = mode == 0 ? a.F : a.H;
   const int rows_s = mode == 0 ? a.Fs : a.H;
-  return (a.S > 0 ? a.S * (rows_s / rows_per_block) : 0) + a.E * (rows_r / rows_per_block);
+  const int slots = a.E < a.B * a.k ? a.E : a.B * a.k;
+  return (a.S > 0 ? a.S * (rows_s / rows_per_block) : 0) + slots * (rows_r / rows_per_block);
 }
 
 }  // namespace ffn

@@ -14,6 +14,21 @@ namespace s2moe {
 
 namespace {
 
+// Dot product of one 16-byte chunk of a token row and of a router row.
+template <bool kBf16>
+__device__ __forceinline__ float dot_chunk(u32x4 xc, u32x4 wc, float acc) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    if (kBf16) {
+      acc = fmaf(bf16_to_f32(wc[i] & 0xFFFFu), bf16_to_f32(xc[i] & 0xFFFFu), acc);
+      acc = fmaf(bf16_to_f32(wc[i] >> 16), bf16_to_f32(xc[i] >> 16), acc);
+    } else {
+      acc = fmaf(__uint_as_float(wc[i]), __uint_as_float(xc[i]), acc);
+    }
+  }
+  return acc;
+}
+
 // Partial dot products of the token row with 4 router rows (e0 .. e0+3,
 // those < E) over the 16-byte chunks [c_lo, c_hi) of H: lanes split the
 // chunks, so up to 4 iterations x 5 loads are in flight together.
@@ -35,19 +50,7 @@ __device__ __forceinline__ void dot_rows4(const char* x, const char* w, int H, i
 #pragma unroll
     for (int q = 0; q < 4; ++q) wc[q] = wr[q][c];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      if (kBf16) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          acc[q] = fmaf(bf16_to_f32(wc[q][i] & 0xFFFFu), bf16_to_f32(xc[i] & 0xFFFFu), acc[q]);
-          acc[q] = fmaf(bf16_to_f32(wc[q][i] >> 16), bf16_to_f32(xc[i] >> 16), acc[q]);
-        }
-      } else {
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-          acc[q] = fmaf(__uint_as_float(wc[q][i]), __uint_as_float(xc[i]), acc[q]);
-      }
-    }
+    for (int q = 0; q < 4; ++q) acc[q] = dot_chunk<kBf16>(xc, wc[q], acc[q]);
   }
 #pragma unroll
   for (int q = 0; q < 4; ++q) acc[q] = wave_sum_dpp(acc[q]);
@@ -62,6 +65,70 @@ __host__ __device__ inline int route_slices(int E, int chunks) {
   return S;
 }
 
+// Plain top-k and gap of token b from its E logits in ell_s (rank_s
+// zeroed and every thread past a barrier): rank every logit (value desc,
+// expert id asc), take ranks 0..k-1 in id order, gap = rank 0 - rank k.
+__device__ void select_plain(const RouteArgs& a, int b, const float* ell_s, int* rank_s,
+                             float* top1_s, float* kth1_s) {
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), E = a.E, k = a.k;
+  block_rank_desc(ell_s, E, rank_s, tid, blockDim.x);
+  __syncthreads();
+  if (tid < E) {
+    if (rank_s[tid] == 0) *top1_s = ell_s[tid];
+    if (rank_s[tid] == k) *kth1_s = ell_s[tid];
+  }
+  __syncthreads();
+  if (wave_id() != 0) return;
+  uint32_t bits = 0;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int e = lane + kWave * j;
+    if (e < E && rank_s[e] < k) bits |= 1u << j;
+  }
+  int rank[4];
+  wave_rank_flagged<4>(bits, rank);
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+    if ((bits >> j) & 1u) a.plain_idx[(size_t)b * k + rank[j]] = lane + kWave * j;
+  if (lane == 0) a.gap[b] = *top1_s - *kth1_s;
+}
+
+// Small batches: one wave per router row computes that expert's logit for
+// every token, so the E rows are streamed by E waves spread over the GPU
+// instead of by one workgroup per token.  Lanes take 16-byte chunks of H;
+// a DPP reduction adds them.
+template <bool kBf16>
+__global__ __launch_bounds__(256) void route_rows_kernel(RouteArgs a) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int e = blockIdx.x * 4 + wave_id();
+  if (e >= a.E) return;
+  const size_t row = (size_t)a.H * (kBf16 ? 2 : 4);
+  const u32x4* wr = reinterpret_cast<const u32x4*>(static_cast<const char*>(a.router) + e * row);
+  const int chunks = a.H / (kBf16 ? 8 : 4);
+  for (int b = 0; b < a.B; ++b) {
+    const u32x4* xr = reinterpret_cast<const u32x4*>(static_cast<const char*>(a.x) + b * row);
+    float acc = 0.f;
+#pragma unroll 4
+    for (int c = lane; c < chunks; c += kWave) acc = dot_chunk<kBf16>(xr[c], wr[c], acc);
+    acc = wave_sum_dpp(acc);
+    if (lane == 0) a.logits[(size_t)b * a.E + e] = acc;
+  }
+}
+
+// Plain top-k and gap of each token from the logits route_rows_kernel wrote.
+__global__ __launch_bounds__(256) void route_select_kernel(RouteArgs a) {
+  __shared__ float ell_s[kMaxExperts];
+  __shared__ int rank_s[kMaxExperts];
+  __shared__ float top1_s, kth1_s;
+  const int b = blockIdx.x, tid = threadIdx.x;
+  if (tid < a.E) {
+    ell_s[tid] = a.logits[(size_t)b * a.E + tid];
+    rank_s[tid] = 0;
+  }
+  __syncthreads();
+  select_plain(a, b, ell_s, rank_s, &top1_s, &kth1_s);
+}
+
 template <bool kBf16>
 __global__ __launch_bounds__(1024) void route_kernel(RouteArgs a) {
   __shared__ float part_s[kMaxExperts];  // [slice][E]: slices * E <= 256
@@ -73,7 +140,7 @@ __global__ __launch_bounds__(1024) void route_kernel(RouteArgs a) {
   const int wave = wave_id();
   const int n_waves = blockDim.x >> 6;
   const int b = blockIdx.x;
-  const int H = a.H, E = a.E, k = a.k;
+  const int H = a.H, E = a.E;
   const char* xb = static_cast<const char*>(a.x) + (size_t)b * H * (kBf16 ? 2 : 4);
   const char* wr = static_cast<const char*>(a.router);
   const int chunks = H / (kBf16 ? 8 : 4);
@@ -102,33 +169,29 @@ __global__ __launch_bounds__(1024) void route_kernel(RouteArgs a) {
     a.logits[(size_t)b * E + tid] = v;
   }
   __syncthreads();
-  // Rank of every logit (value desc, expert id asc); the plain top-k are
-  // ranks 0..k-1 and ell_(k+1) is the value of rank k.
-  block_rank_desc(ell_s, E, rank_s, tid, blockDim.x);
-  __syncthreads();
-  if (tid < E) {
-    if (rank_s[tid] == 0) top1_s = ell_s[tid];
-    if (rank_s[tid] == k) kth1_s = ell_s[tid];
-  }
-  __syncthreads();
-  if (wave != 0) return;
-  uint32_t bits = 0;
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int e = lane + kWave * j;
-    if (e < E && rank_s[e] < k) bits |= 1u << j;
-  }
-  int rank[4];
-  wave_rank_flagged<4>(bits, rank);
-#pragma unroll
-  for (int j = 0; j < 4; ++j)
-    if ((bits >> j) & 1u) a.plain_idx[(size_t)b * k + rank[j]] = lane + kWave * j;
-  if (lane == 0) a.gap[b] = top1_s - kth1_s;
+  select_plain(a, b, ell_s, rank_s, &top1_s, &kth1_s);
 }
 
 }  // namespace
 
+// Below this many tokens the router rows are spread over the GPU (two
+// launches) instead of one workgroup per token.
+#ifndef S2MOE_ROUTE_ROWS_MAX_B
+#define S2MOE_ROUTE_ROWS_MAX_B 8
+#endif
+
 hipError_t launch_route(const RouteArgs& a, hipStream_t s) {
+  if (a.B <= S2MOE_ROUTE_ROWS_MAX_B) {
+    const dim3 grid((a.E + 3) / 4);
+    if (a.bf16)
+      hipLaunchKernelGGL(route_rows_kernel<true>, grid, dim3(256), 0, s, a);
+    else
+      hipLaunchKernelGGL(route_rows_kernel<false>, grid, dim3(256), 0, s, a);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(route_select_kernel, dim3(a.B), dim3(256), 0, s, a);
+    return hipGetLastError();
+  }
   // One wave per (H slice, 4 experts) item, at most 16; E <= 256 keeps at
   // least one thread per expert for the ranking.
   const int chunks = a.H / (a.bf16 ? 8 : 4);
