@@ -110,6 +110,24 @@ def test_max_experts_and_topk():
     _full_check(shape, d, "E=256 k=16")
 
 
+def test_max_tokens_experts_and_topk_together():
+    """B = 256 with E = 256 and k = 16: 4096 assignments, logits too many
+    to stage in LDS, every bucket-building path at its largest."""
+    shape = LayerShape(hidden=128, ffn=128, n_experts=256, top_k=16, cap=48, alpha=0.5)
+    d = make_inputs(shape, 256, seed=12, rho=0.5)
+    got, _ = _full_check(shape, d, "B=256 E=256 k=16")
+    assert got["count"].sum() == 256 * 16
+
+
+def test_max_hidden():
+    """H = 16384 (the documented maximum): long router rows and gate-up
+    rows, bf16, small B."""
+    shape = LayerShape(hidden=16384, ffn=256, n_experts=8, top_k=2, cap=4, alpha=0.5)
+    for B in (3, 40):
+        d = make_inputs(shape, B, seed=13 + B, rho=0.5)
+        _full_check(shape, d, f"H=16384 B={B}")
+
+
 def test_cap_equal_E_and_identical_tokens():
     shape = LayerShape(hidden=256, ffn=256, n_experts=16, top_k=3, cap=16, alpha=0.9)
     d = make_inputs(shape, 12, seed=5, rho=0.5)
