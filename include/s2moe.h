@@ -82,11 +82,13 @@ enum {
    (BF16, BF16), (BF16, Q4G32). */
 typedef struct s2moe_layer {
   int32_t hidden;      /* H: 64 <= H <= 16384, H % 64 == 0                  */
-  int32_t ffn;         /* F: routed SwiGLU width, 64 <= F, F % 64 == 0      */
+  int32_t ffn;         /* F: routed SwiGLU width, 64 <= F <= 262144,
+                          F % 64 == 0 (F % 256 == 0 with Q4G32 weights,
+                          like H and F_s)                                   */
   int32_t n_experts;   /* E: 2 <= E <= 256                                  */
   int32_t top_k;       /* k: 1 <= k < E, k <= 16                            */
   int32_t n_shared;    /* S: 0 <= S <= 8 always-on experts (weight 1)       */
-  int32_t ffn_shared;  /* F_s: F_s % 64 == 0 when S > 0                     */
+  int32_t ffn_shared;  /* F_s: 64 <= F_s <= 262144, F_s % 64 == 0 when S > 0 */
   int32_t cap;         /* k <= cap <= E                                     */
   float alpha;         /* lambda_b = alpha * gap_b, alpha >= 0, finite      */
   uint32_t flags;      /* S2MOE_PREF_ACTIVATED_ONLY | ... (default 0)       */

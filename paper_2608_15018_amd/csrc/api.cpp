@@ -43,8 +43,8 @@ s2moe_status check_layer(const char* fn, const s2moe_layer* L, int32_t B) {
   if (B < 1) return fail(S2MOE_EINVAL, "%s: n_tokens = %d, must be >= 1", fn, B);
   if (B > S2MOE_MAX_TOKENS)
     return fail(S2MOE_EUNSUPPORTED, "%s: n_tokens = %d exceeds %d", fn, B, S2MOE_MAX_TOKENS);
-  if (L->hidden < 64 || L->hidden % 64 != 0 || L->hidden > 65536)
-    return fail(S2MOE_EINVAL, "%s: hidden = %d must be a multiple of 64 in [64, 65536]", fn,
+  if (L->hidden < 64 || L->hidden % 64 != 0 || L->hidden > 16384)
+    return fail(S2MOE_EINVAL, "%s: hidden = %d must be a multiple of 64 in [64, 16384]", fn,
                 L->hidden);
   if (L->ffn < 64 || L->ffn % 64 != 0 || L->ffn > 262144)
     return fail(S2MOE_EINVAL, "%s: ffn = %d must be a multiple of 64 in [64, 262144]", fn,

@@ -68,6 +68,8 @@ def _route_status(lib, layer, B=4, ptrs=True):
     ({"act": "f32", "wdt": "bf16"}, 4, _lib.EUNSUPPORTED, "supported"),
     ({"act": "q4g32"}, 4, _lib.EINVAL, "act_dtype"),
     ({"wdt": "q4g32", "ffn": 320}, 4, _lib.EUNSUPPORTED, "Q4G32"),
+    ({"hidden": 16384 + 64}, 4, _lib.EINVAL, "hidden"),
+    ({"ffn": 262144 + 64}, 4, _lib.EINVAL, "ffn"),
 ])
 def test_invalid_layers_rejected_on_host(lib, kw, B, status, needle):
     st, msg = _route_status(lib, _layer(**kw), B)
