@@ -83,7 +83,7 @@ enum {
 typedef struct s2moe_layer {
   int32_t hidden;      /* H: 64 <= H <= 16384, H % 64 == 0                  */
   int32_t ffn;         /* F: routed SwiGLU width, 64 <= F <= 262144,
-                          F % 64 == 0 (F % 256 == 0 with Q4G32 weights,
+                          F % 64 == 0 (F % 128 == 0 with Q4G32 weights,
                           like H and F_s)                                   */
   int32_t n_experts;   /* E: 2 <= E <= 256                                  */
   int32_t top_k;       /* k: 1 <= k < E, k <= 16                            */

@@ -85,10 +85,12 @@ s2moe_status check_layer(const char* fn, const s2moe_layer* L, int32_t B) {
                 "%s: (act_dtype, w_dtype) = (%d, %d); supported: (F32, F32), (BF16, BF16), "
                 "(BF16, Q4G32)",
                 fn, act, wdt);
+  // int4 kernels step through K in 128-wide super-steps and take up to 8
+  // 16-row tiles per wave.
   if (wdt == S2MOE_Q4G32 &&
-      (L->hidden % 256 || L->ffn % 256 || (L->n_shared > 0 && L->ffn_shared % 256)))
+      (L->hidden % 128 || L->ffn % 128 || (L->n_shared > 0 && L->ffn_shared % 128)))
     return fail(S2MOE_EUNSUPPORTED,
-                "%s: Q4G32 weights need hidden, ffn and ffn_shared multiples of 256", fn);
+                "%s: Q4G32 weights need hidden, ffn and ffn_shared multiples of 128", fn);
   if ((L->flags & S2MOE_PACKED_WEIGHTS) && wdt == S2MOE_F32)
     return fail(S2MOE_EUNSUPPORTED, "%s: S2MOE_PACKED_WEIGHTS needs BF16 or Q4G32 weights", fn);
   return S2MOE_OK;

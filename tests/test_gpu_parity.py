@@ -119,6 +119,27 @@ def test_max_tokens_experts_and_topk_together():
     assert got["count"].sum() == 256 * 16
 
 
+def test_int4_deepseek_shaped_with_shared():
+    """int4 weights at the DeepSeek-V2-Lite expert width F = F_s = 1408
+    (11 super-steps of 128, not a power of two) with 2 shared experts,
+    packed and row-major, at 4 and 64 tokens."""
+    shape = LayerShape(hidden=512, ffn=1408, n_experts=16, top_k=6, n_shared=2, ffn_shared=1408,
+                       cap=12, alpha=0.5, act="bf16", wdt="q4g32")
+    for B in (4, 64):
+        d = make_inputs(shape, B, seed=21 + B, rho=0.4)
+        deq = lambda ex: {n: np.stack([oracle.dequant_q4g32(ex[n][e], ex[n + "_s"][e])  # noqa: E731
+                                       for e in range(ex[n].shape[0])]).astype(np.float32)
+                          for n in ("gate", "up", "down")}
+        log(f"[parity] int4 F=1408 shared B={B}")
+        got, _ = run_gpu(shape, d)
+        packed, _ = run_gpu(shape, d, packed=True)
+        assert np.array_equal(packed["expert_out"], got["expert_out"])
+        ref = oracle.forward(d["x"], d["router"], d["conf_w"], deq(d["experts"]),
+                             deq(d["shared"]), shape.with_(wdt="f32"))
+        check_routing(got, ref, f"int4 F=1408 B={B}")
+        check_outputs(got, ref, "q4g32", f"int4 F=1408 B={B}")
+
+
 def test_max_hidden():
     """H = 16384 (the documented maximum): long router rows and gate-up
     rows, bf16, small B."""
