@@ -346,7 +346,7 @@ hipError_t launch_q4_mode(const FfnArgs& a, hipStream_t s) {
 #define S2MOE_Q4_MEDIUM 2, 1, 2
 #endif
 #ifndef S2MOE_Q4_LARGE
-#define S2MOE_Q4_LARGE 2, 2, 2
+#define S2MOE_Q4_LARGE 2, 2, 4
 #endif
 
 template <int TMAX, int RG, int RD>
