@@ -96,7 +96,45 @@ __device__ __forceinline__ int count_new(const uint32_t* a, const uint32_t* b) {
   return c;
 }
 
-template <int NPT, int EW>
+// Where tree t's ids lie: n * L * k int32 from element e0 of eid (n = the
+// tree's node count, clamped to [0, N]); the first `head` ids precede the
+// first 16-byte boundary, then `nch` whole 16-byte chunks, then the rest.
+struct IdRun {
+  int n, bad_count, total, head, nch;
+  size_t e0;
+};
+
+__device__ __forceinline__ IdRun id_run(const ExpandArgs& a, int t) {
+  IdRun r;
+  const int n = a.n_nodes[t];
+  r.bad_count = n < 0 || n > a.N;
+  r.n = min(max(n, 0), a.N);
+  r.e0 = (size_t)t * a.N * (size_t)(a.L * a.k);
+  r.total = r.n * a.L * a.k;
+  // eid is 16-byte aligned, so the run's first 16-byte boundary is at
+  // element (4 - e0 mod 4) mod 4.
+  r.head = min(r.total, (int)((4u - (uint32_t)(r.e0 & 3u)) & 3u));
+  r.nch = (r.total - r.head) >> 2;
+  return r;
+}
+
+// Chunks c = tid + 256 u (u < PF) of a tree's run, loaded ahead.
+template <int PF>
+__device__ __forceinline__ void prefetch_ids(const ExpandArgs& a, const IdRun& r, u32x4 (&pf)[PF]) {
+  const u32x4* body = reinterpret_cast<const u32x4*>(a.eid + r.e0 + r.head);
+#pragma unroll
+  for (int u = 0; u < PF; ++u) {
+    const int c = (int)threadIdx.x + u * kThreads;
+    if (c < r.nch) pf[u] = __builtin_nontemporal_load(body + c);
+  }
+}
+
+// A persistent workgroup takes trees blockIdx.x, + gridDim.x, ...  With
+// PF > 0, while it runs one tree's greedy loop the first PF * 256 chunks of
+// its next tree's ids are already on their way into registers (used when a
+// tree's LDS leaves room for one workgroup per CU anyway; smaller trees run
+// several workgroups per CU instead).
+template <int NPT, int EW, int PF>
 __global__ __launch_bounds__(kThreads) void expand_kernel(ExpandArgs a) {
   extern __shared__ __align__(16) unsigned char lds[];
   const ExpandLds lay = expand_lds(a.N, a.L, a.E, a.k);
@@ -108,19 +146,22 @@ __global__ __launch_bounds__(kThreads) void expand_kernel(ExpandArgs a) {
   Misc* misc = reinterpret_cast<Misc*>(lds + lay.misc);
   uint8_t* state = lds + lay.state;
 
-  const int t = blockIdx.x;
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
   const int L = a.L, E = a.E, k = a.k, N = a.N;
   const int Lk = L * k;
-  const size_t node0 = (size_t)t * N;
 
-  int n = a.n_nodes[t];
-  int status = 0;
-  if (n < 0 || n > N) {
-    status |= 8;
-    n = min(max(n, 0), N);
-  }
+  u32x4 pf[PF > 0 ? PF : 1];
+  if constexpr (PF > 0)
+    if ((int)blockIdx.x < a.T) prefetch_ids<PF>(a, id_run(a, blockIdx.x), pf);
+
+  // Without prefetch the grid has one workgroup per tree: one pass.
+  const int t_step = PF > 0 ? (int)gridDim.x : a.T;
+  for (int t = blockIdx.x; t < a.T; t += t_step) {
+  const size_t node0 = (size_t)t * N;
+  const IdRun run = id_run(a, t);
+  const int n = run.n;
+  int status = run.bad_count ? 8 : 0;
 
   // (1) per-node records and the root's ids: one round of loads.
   int par[NPT];
@@ -186,9 +227,7 @@ __global__ __launch_bounds__(kThreads) void expand_kernel(ExpandArgs a) {
   // (2) the tree's ids, one contiguous node-major run of n * L * k int32:
   // id f belongs to row f / k (= node * L + layer); ids outside [0, E) are
   // padding.
-  const size_t e0 = node0 * (size_t)Lk;
-  const int total = n * Lk;
-  const int32_t* src = a.eid + e0;
+  const int32_t* src = a.eid + run.e0;
   // Sets bit e of the row's bitset; padding ORs 0 into word 0 (no branch).
   auto set_bit = [&](uint32_t row, int e) {
     const bool ok = (uint32_t)e < (uint32_t)E;
@@ -196,16 +235,39 @@ __global__ __launch_bounds__(kThreads) void expand_kernel(ExpandArgs a) {
     atomicOr(&rows[w], ok ? 1u << (e & 31) : 0u);
   };
   auto row_of = [&](uint32_t f) { return (uint32_t)(((uint64_t)f * a.k_div) >> 42); };
-  // eid is 16-byte aligned, so the run's first 16-byte boundary is at
-  // element (4 - e0 mod 4) mod 4.
-  const int head = min(total, (int)((4u - (uint32_t)(e0 & 3u)) & 3u));
+  const int head = run.head, nch = run.nch;
   for (int f = tid; f < head; f += kThreads) set_bit(row_of(f), src[f]);
-  const int nch = (total - head) >> 2;
   const u32x4* body = reinterpret_cast<const u32x4*>(src + head);
   // With head == 0 and k a multiple of 4, the four ids of a chunk share a row.
   const bool same_row = head == 0 && (k & 3) == 0;
-  constexpr int kBatch = 32;
-  for (int c0 = 0; c0 < nch; c0 += kThreads * kBatch) {
+  auto place_chunk = [&](int c, const u32x4& v) {
+    const uint32_t f = head + 4 * c;
+    uint32_t row = row_of(f);
+    if (same_row) {
+#pragma unroll
+      for (int x = 0; x < 4; ++x) set_bit(row, (int)v[x]);
+    } else {
+      uint32_t pos = f - row * k;  // position of the first id in its row
+#pragma unroll
+      for (int x = 0; x < 4; ++x) {
+        set_bit(row, (int)v[x]);
+        if (++pos == (uint32_t)k) {
+          pos = 0;
+          ++row;
+        }
+      }
+    }
+  };
+  // The prefetched chunks, then the rest of the run in batches.
+  if constexpr (PF > 0) {
+#pragma unroll
+    for (int u = 0; u < PF; ++u) {
+      const int c = tid + u * kThreads;
+      if (c < nch) place_chunk(c, pf[u]);
+    }
+  }
+  constexpr int kBatch = 16;
+  for (int c0 = PF * kThreads; c0 < nch; c0 += kThreads * kBatch) {
     u32x4 v[kBatch];
 #pragma unroll
     for (int u = 0; u < kBatch; ++u) {
@@ -215,27 +277,13 @@ __global__ __launch_bounds__(kThreads) void expand_kernel(ExpandArgs a) {
 #pragma unroll
     for (int u = 0; u < kBatch; ++u) {
       const int c = c0 + tid + u * kThreads;
-      if (c < nch) {
-        const uint32_t f = head + 4 * c;
-        uint32_t row = row_of(f);
-        if (same_row) {
-#pragma unroll
-          for (int x = 0; x < 4; ++x) set_bit(row, (int)v[u][x]);
-        } else {
-          uint32_t pos = f - row * k;  // position of the first id in its row
-#pragma unroll
-          for (int x = 0; x < 4; ++x) {
-            set_bit(row, (int)v[u][x]);
-            if (++pos == (uint32_t)k) {
-              pos = 0;
-              ++row;
-            }
-          }
-        }
-      }
+      if (c < nch) place_chunk(c, v[u]);
     }
   }
-  for (int f = head + 4 * nch + tid; f < total; f += kThreads) set_bit(row_of(f), src[f]);
+  for (int f = head + 4 * nch + tid; f < run.total; f += kThreads) set_bit(row_of(f), src[f]);
+  // This tree's ids are placed: start loading the next tree's.
+  if constexpr (PF > 0)
+    if (t + t_step < a.T) prefetch_ids<PF>(a, id_run(a, t + t_step), pf);
 
   // (3) prefix confidences, root-down: p_i = p_parent * q_i.  Each pass
   // reads resolved parents, then (after a barrier) writes, so no value is
@@ -375,18 +423,39 @@ __global__ __launch_bounds__(kThreads) void expand_kernel(ExpandArgs a) {
     a.n_pairs[t] = misc->pairs;
     a.status[t] = misc->status;
   }
+  }  // trees
 }
+
+template <int NPT, int EW, int PF>
+hipError_t launch_pf(const ExpandArgs& a, size_t lds_bytes, hipStream_t s) {
+  const void* fn = reinterpret_cast<const void*>(&expand_kernel<NPT, EW, PF>);
+  if (lds_bytes > 65536) {
+    const hipError_t e =
+        hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_bytes);
+    if (e != hipSuccess) return e;
+  }
+  // With prefetch, one persistent workgroup per resident slot (at most one
+  // per tree); without, one workgroup per tree.
+  int grid = a.T;
+  if (PF > 0) {
+    int per_cu = 0, dev = 0, cus = 0;
+    hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kThreads, lds_bytes);
+    if (e == hipSuccess) e = hipGetDevice(&dev);
+    if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return e;
+    grid = max(1, min(a.T, max(1, per_cu) * cus));
+  }
+  hipLaunchKernelGGL((expand_kernel<NPT, EW, PF>), dim3(grid), dim3(kThreads), lds_bytes, s, a);
+  return hipGetLastError();
+}
+
+// Prefetch only when a tree's LDS already limits a CU to one workgroup.
+constexpr size_t kLdsPerCu = 160 * 1024;
 
 template <int NPT, int EW>
 hipError_t launch_ew(const ExpandArgs& a, size_t lds_bytes, hipStream_t s) {
-  if (lds_bytes > 65536) {
-    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&expand_kernel<NPT, EW>),
-                                             hipFuncAttributeMaxDynamicSharedMemorySize,
-                                             (int)lds_bytes);
-    if (e != hipSuccess) return e;
-  }
-  hipLaunchKernelGGL((expand_kernel<NPT, EW>), dim3(a.T), dim3(kThreads), lds_bytes, s, a);
-  return hipGetLastError();
+  return 2 * lds_bytes > kLdsPerCu ? launch_pf<NPT, EW, 32>(a, lds_bytes, s)
+                                   : launch_pf<NPT, EW, 0>(a, lds_bytes, s);
 }
 
 template <int NPT>
