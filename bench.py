@@ -118,25 +118,19 @@ def recorded_expand_traffic(name: str, trees: int):
                            expand_source_hash())
 
 
-def recorded_traffic(name: str, wdt: str):
+def recorded_traffic(name: str, wdt: str, B: int, default_B: int):
     """HBM bytes per s2moe_verify_moe call from the committed rocprofv3 counter
-    summary of this workload, or None if there is none or the kernel sources
-    changed since it was taken."""
-    path = os.path.join(ROOT, "profiles", f"verify_moe_{name}_traffic.md")
-    if not os.path.exists(path):
-        return None
-    vals = {}
-    with open(path) as f:
-        for line in f:
-            k, _, v = line.strip().lstrip("- ").partition(":")
-            if k in ("traffic_bytes_per_launch", "kernel_source_sha256"):
-                vals[k] = v.strip().strip("`")
-    if vals.get("kernel_source_sha256") != ffn_source_hash(wdt):
-        return None
-    try:
-        return int(vals["traffic_bytes_per_launch"])
-    except (KeyError, ValueError):
-        return None
+    summary of this workload at B draft tokens (verify_moe_<name>_b<B>_traffic.md,
+    or verify_moe_<name>_traffic.md at the workload's default B), or None if
+    there is none or the kernel sources changed since it was taken."""
+    names = [f"verify_moe_{name}_b{B}_traffic.md"]
+    if B == default_B:
+        names.append(f"verify_moe_{name}_traffic.md")
+    for n in names:
+        v = _traffic_record(os.path.join(ROOT, "profiles", n), ffn_source_hash(wdt))
+        if v is not None:
+            return v
+    return None
 
 
 def _head_start():
@@ -453,7 +447,8 @@ def main(argv=None):
         return bench_draft(args)
     wl = WORKLOADS[args.workload]
     shape = wl.shape if args.alpha is None else wl.shape.with_(alpha=args.alpha)
-    B = args.batch or wl.batches[-1 if args.workload == "c5" else 0]
+    default_B = wl.batches[-1 if args.workload == "c5" else 0]
+    B = args.batch or default_B
     wid = WORKLOAD_ID[wl.name]
 
     t0 = time.time()
@@ -571,7 +566,7 @@ def main(argv=None):
                    "alpha": shape.alpha, "weights": "packed" if packed else "row-major"},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
-                     "traffic": recorded_traffic(wl.name, shape.wdt),
+                     "traffic": recorded_traffic(wl.name, shape.wdt, B, default_B),
                      "kernel": "s2moe_verify_moe (expert gate-up + down launches)",
                      "bytes_per_launch": unique_bytes, "avg_launch_us": ffn_avg_s * 1e6},
         "cpu_baseline": cpu,

@@ -19,6 +19,8 @@
 //
 // Work decomposition as in the bf16 kernel: R 16-row tiles per unit, W waves
 // split K, two-stage register pipeline, LDS reduction in wave order.
+#include <atomic>
+
 #include "ffn_common.h"
 
 namespace s2moe {
@@ -338,10 +340,11 @@ hipError_t launch_q4_mode(const FfnArgs& a, hipStream_t s) {
 
 // Tile choices per batch size: (TMAX token tiles held at once, row tiles per
 // wave for gate-up, row tiles per wave for down).  Buckets larger than
-// 16 * TMAX tokens take several passes over the same weight rows.
-#ifndef S2MOE_Q4_SMALL
-#define S2MOE_Q4_SMALL 1, 2, 4
-#endif
+// 16 * TMAX tokens take several passes over the same weight rows.  Up to 16
+// tokens one token tile is held, and the row tiles per wave are the most
+// (gate-up 2, down 4) that still give every compute unit a workgroup: with
+// one or two activated experts (a draft step, or B = 1) fewer rows per
+// workgroup spread the weight stream over the whole GPU.
 #ifndef S2MOE_Q4_MEDIUM
 #define S2MOE_Q4_MEDIUM 2, 1, 2
 #endif
@@ -355,6 +358,31 @@ hipError_t launch_q4_pair(const FfnArgs& a, hipStream_t s) {
   return err != hipSuccess ? err : launch_q4_mode<1, TMAX, RD>(a, s);
 }
 
+// Compute units of the current device, queried once per device.
+hipError_t device_cus(int* cus) {
+  static std::atomic<int> cache[64];
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev >= 0 && dev < 64 && (*cus = cache[dev].load(std::memory_order_relaxed)) > 0)
+    return hipSuccess;
+  e = hipDeviceGetAttribute(cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess) return e;
+  if (dev >= 0 && dev < 64) cache[dev].store(*cus, std::memory_order_relaxed);
+  return hipSuccess;
+}
+
+hipError_t launch_q4_small(const FfnArgs& a, hipStream_t s) {
+  int cus = 0;
+  hipError_t err = device_cus(&cus);
+  if (err != hipSuccess) return err;
+  err = n_blocks(a, 0, 32) >= cus ? launch_q4_mode<0, 1, 2>(a, s) : launch_q4_mode<0, 1, 1>(a, s);
+  if (err != hipSuccess) return err;
+  if (n_blocks(a, 1, 64) >= cus) return launch_q4_mode<1, 1, 4>(a, s);
+  if (n_blocks(a, 1, 32) >= cus) return launch_q4_mode<1, 1, 2>(a, s);
+  return launch_q4_mode<1, 1, 1>(a, s);
+}
+
 }  // namespace
 
 hipError_t launch_ffn_q4(const FfnArgs& a, hipStream_t s) {
@@ -363,7 +391,7 @@ hipError_t launch_ffn_q4(const FfnArgs& a, hipStream_t s) {
                      static_cast<const uint16_t*>(a.x), static_cast<uint16_t*>(a.x16), n8);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
-  if (a.B <= 16) return launch_q4_pair<S2MOE_Q4_SMALL>(a, s);
+  if (a.B <= 16) return launch_q4_small(a, s);
   if (a.B <= 32) return launch_q4_pair<S2MOE_Q4_MEDIUM>(a, s);
   return launch_q4_pair<S2MOE_Q4_LARGE>(a, s);
 }
