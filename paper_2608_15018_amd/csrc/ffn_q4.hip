@@ -18,7 +18,9 @@
 // stored so that every B-operand load reads 64 contiguous bytes per token.
 //
 // Work decomposition as in the bf16 kernel: R 16-row tiles per unit, W waves
-// split K, two-stage register pipeline, LDS reduction in wave order.
+// split K, two-stage register pipeline, LDS reduction in wave order.  Above
+// 16 tokens the gate-up launch instead uses a row-split kernel whose waves
+// share LDS-staged activations (ffn_q4_rows_kernel).
 #include <atomic>
 
 #include "ffn_common.h"
@@ -284,6 +286,217 @@ __global__ __launch_bounds__(W * 64) void ffn_q4_kernel(FfnArgs a) {
   }
 }
 
+// Row-split variant for two token tiles: the W = 4 waves of a workgroup take
+// different row tiles over all of K, and share the activations, which the
+// workgroup stages in LDS two super-steps at a time (double-buffered, one
+// barrier per two super-steps).  The B operands then come from LDS instead
+// of one global load per wave, which at two token tiles would move twice the
+// weight bytes through the texture units.
+constexpr int kChunkU4 = 32;       // u32x4 of one token row per chunk (2 super-steps)
+constexpr int kLdsRowU4 = kChunkU4 + 1;  // padded: the 16 rows of a tile hit distinct banks
+
+template <int R, int NM>
+struct CodesQ {
+  u32x4 c[NM][R];
+  uint32_t s[NM][R];
+};
+
+template <bool kPacked, int R, int NM>
+__device__ __forceinline__ void load_codes(CodesQ<R, NM>& st, const u32x4* const* pc,
+                                           const uint16_t* const* ps, int s) {
+#pragma unroll
+  for (int m = 0; m < NM; ++m)
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      if (kPacked) {
+        st.c[m][r] = __builtin_nontemporal_load(pc[m * R + r] + 64 * s);
+        st.s[m][r] = __builtin_nontemporal_load(ps[m * R + r] + 64 * s);
+      } else {
+        st.c[m][r] = pc[m * R + r][4 * s];
+        st.s[m][r] = ps[m * R + r][4 * s];
+      }
+    }
+}
+
+// One super-step: codes from registers, B operands from LDS half h of the
+// staged chunk.
+template <int T, int R, int NM>
+__device__ __forceinline__ void compute_rows(const CodesQ<R, NM>& st, const u32x4* buf, int h,
+                                             f32x4 (&acc)[NM][R][T], uint32_t magic) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int rA = lane & 15, gK = lane >> 4;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    half8v b[T];
+#pragma unroll
+    for (int tt = 0; tt < T; ++tt) b[tt] = as_half8(buf[(tt * 16 + rA) * kLdsRowU4 + 16 * h + 4 * j + gK]);
+#pragma unroll
+    for (int m = 0; m < NM; ++m)
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        _Float16 sh;
+        const uint16_t bits = (uint16_t)st.s[m][r];
+        __builtin_memcpy(&sh, &bits, 2);
+        const half2v s2 = {sh, sh};
+        const half8v a = q4_decode(st.c[m][r][j], s2, magic);
+#pragma unroll
+        for (int tt = 0; tt < T; ++tt) acc[m][r][tt] = mfma16(a, b[tt], acc[m][r][tt]);
+      }
+  }
+}
+
+template <int kMode, int T, int R, int W, bool kPacked>
+__device__ __forceinline__ void rows_pass_q(const FfnArgs& a, const Segment& seg, int t0, int r0,
+                                            int K, const uint8_t* C0, const uint8_t* C1,
+                                            const uint16_t* S0, const uint16_t* S1, u32x4* lds) {
+  constexpr int NM = kMode == 0 ? 2 : 1;
+  constexpr int kBuf = T * 16 * kLdsRowU4;       // u32x4 per LDS buffer
+  constexpr int kStg = T * 16 * kChunkU4 / (W * kWave);  // staged u32x4 per thread
+  const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1);
+  const int wave = wave_id();
+  const int rA = lane & 15, gK = lane >> 4;
+  const int nss = K / 128, nch = (nss + 1) / 2;
+  const int rw = r0 + wave * 16 * R;  // the wave's first row
+
+  // Staging map: thread item q covers token row tok, 16-byte block blk of the
+  // chunk (16 blocks per super-step).
+  const uint16_t* X = static_cast<const uint16_t*>(kMode == 0 ? a.x16 : a.hh);
+  const int ldx = kMode == 0 ? a.H : a.ldh;
+  const u32x4* xs[kStg];
+  int ld_off[kStg], blk_h[kStg], blk_l[kStg];
+#pragma unroll
+  for (int q = 0; q < kStg; ++q) {
+    const int idx = tid + q * W * kWave;
+    const int tok = idx / kChunkU4, blk = idx % kChunkU4;
+    const int t = min(t0 + tok, seg.n - 1);
+    xs[q] = reinterpret_cast<const u32x4*>(X + (size_t)x_row(a, kMode, seg, t) * ldx);
+    ld_off[q] = tok * kLdsRowU4 + blk;
+    blk_h[q] = blk >> 4;
+    blk_l[q] = blk & 15;
+  }
+  // Chunk c holds super-steps 2c and 2c + 1 (the latter clamped to the last).
+  auto load_stage = [&](u32x4 (&v)[kStg], int c) {
+#pragma unroll
+    for (int q = 0; q < kStg; ++q) v[q] = xs[q][16 * min(2 * c + blk_h[q], nss - 1) + blk_l[q]];
+  };
+  auto store_stage = [&](const u32x4 (&v)[kStg], u32x4* buf) {
+#pragma unroll
+    for (int q = 0; q < kStg; ++q) buf[ld_off[q]] = v[q];
+  };
+
+  const u32x4* pc[NM * R];
+  const uint16_t* ps[NM * R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    if (kPacked) {
+      const size_t tile0 = (size_t)(rw / 16 + r) * nss;
+      pc[r] = reinterpret_cast<const u32x4*>(C0) + tile0 * 64 + lane;
+      ps[r] = S0 + tile0 * 64 + lane;
+      if (NM > 1) {
+        pc[R + r] = reinterpret_cast<const u32x4*>(C1) + tile0 * 64 + lane;
+        ps[R + r] = S1 + tile0 * 64 + lane;
+      }
+    } else {
+      const size_t row = (size_t)(rw + 16 * r + rA);
+      pc[r] = reinterpret_cast<const u32x4*>(C0 + row * (K / 2)) + gK;
+      ps[r] = S0 + row * (K / 32) + gK;
+      if (NM > 1) {
+        pc[R + r] = reinterpret_cast<const u32x4*>(C1 + row * (K / 2)) + gK;
+        ps[R + r] = S1 + row * (K / 32) + gK;
+      }
+    }
+  }
+
+  f32x4 acc[NM][R][T];
+#pragma unroll
+  for (int m = 0; m < NM; ++m)
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+#pragma unroll
+      for (int tt = 0; tt < T; ++tt) acc[m][r][tt] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  const uint32_t magic = opaque(0x64006400u);
+  u32x4 stg[kStg];
+  CodesQ<R, NM> cA, cB;
+  load_stage(stg, 0);
+  load_codes<kPacked>(cA, pc, ps, 0);
+  store_stage(stg, lds);
+  __syncthreads();
+  for (int c = 0; c < nch; ++c) {
+    const u32x4* buf = lds + (c & 1) * kBuf;
+    load_stage(stg, min(c + 1, nch - 1));
+    load_codes<kPacked>(cB, pc, ps, min(2 * c + 1, nss - 1));
+    pipe_barrier();
+    compute_rows(cA, buf, 0, acc, magic);
+    load_codes<kPacked>(cA, pc, ps, min(2 * c + 2, nss - 1));
+    pipe_barrier();
+    if (2 * c + 1 < nss) compute_rows(cB, buf, 1, acc, magic);
+    // The other buffer was last read in chunk c - 1, before the barrier that
+    // ended it.
+    store_stage(stg, lds + ((c + 1) & 1) * kBuf);
+    __syncthreads();
+  }
+
+#pragma unroll
+  for (int tt = 0; tt < T; ++tt) {
+    const int t = t0 + tt * 16 + rA;
+    if (t >= seg.n) continue;
+    if (kMode == 0) {
+      _Float16* dst = static_cast<_Float16*>(a.hh) + (size_t)(seg.base + t) * a.ldh;
+#pragma unroll
+      for (int r = 0; r < R; ++r)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int f = rw + 16 * r + 4 * gK + i;
+          dst[(block_pos(f >> 3) << 3) | pos8(f & 7)] =
+              (_Float16)(silu(acc[0][r][tt][i]) * acc[NM - 1][r][tt][i]);
+        }
+    } else {
+      float* dst = a.out + (size_t)out_row(a, seg, t) * a.H;
+#pragma unroll
+      for (int r = 0; r < R; ++r)
+        *reinterpret_cast<f32x4*>(dst + rw + 16 * r + 4 * gK) = acc[0][r][tt];
+    }
+  }
+}
+
+template <int kMode, int R, int W, bool kPacked>
+__global__ __launch_bounds__(W * 64) void ffn_q4_rows_kernel(FfnArgs a) {
+  // Row counts are multiples of 128, so a workgroup's rows must divide 128.
+  static_assert(128 % (16 * R * W) == 0, "rows per workgroup must divide 128");
+  constexpr int NM = kMode == 0 ? 2 : 1;
+  __shared__ u32x4 lds[2 * 2 * 16 * kLdsRowU4];
+  Segment seg;
+  int unit;
+  if (!resolve_block(a, kMode, 16 * R * W, &seg, &unit)) return;
+  const int r0 = unit * 16 * R * W;
+  const int rows = kMode == 0 ? (seg.shared ? a.Fs : a.F) : a.H;
+  const int K = kMode == 0 ? a.H : (seg.shared ? a.Fs : a.F);
+  const size_t mat = (size_t)rows * K;
+  const void *M0, *M1, *Q0, *Q1;
+  if (kMode == 0) {
+    M0 = seg.shared ? a.sh_gate : a.gate;
+    M1 = seg.shared ? a.sh_up : a.up;
+    Q0 = seg.shared ? a.sh_gate_s : a.gate_s;
+    Q1 = seg.shared ? a.sh_up_s : a.up_s;
+  } else {
+    M0 = M1 = seg.shared ? a.sh_down : a.down;
+    Q0 = Q1 = seg.shared ? a.sh_down_s : a.down_s;
+  }
+  const uint8_t* C0 = static_cast<const uint8_t*>(M0) + seg.id * (mat / 2);
+  const uint8_t* C1 = static_cast<const uint8_t*>(M1) + seg.id * (mat / 2);
+  const uint16_t* S0 = static_cast<const uint16_t*>(Q0) + seg.id * (mat / 32);
+  const uint16_t* S1 = static_cast<const uint16_t*>(Q1) + seg.id * (mat / 32);
+  for (int t0 = 0; t0 < seg.n; t0 += 32) {
+    if (seg.n - t0 > 16)
+      rows_pass_q<kMode, 2, R, W, kPacked>(a, seg, t0, r0, K, C0, C1, S0, S1, lds);
+    else
+      rows_pass_q<kMode, 1, R, W, kPacked>(a, seg, t0, r0, K, C0, C1, S0, S1, lds);
+  }
+  (void)NM;
+}
+
 // x [B, H] bf16 -> x16 [B, H] fp16 in the kernels' order (block_pos, then
 // decode order inside each block), one 8-block per thread (H % 128 == 0, so
 // a row holds whole super-steps).
@@ -338,26 +551,6 @@ hipError_t launch_q4_mode(const FfnArgs& a, hipStream_t s) {
                   : launch_q4_mode_p<kMode, TMAX, R, false>(a, s);
 }
 
-// Tile choices per batch size: (TMAX token tiles held at once, row tiles per
-// wave for gate-up, row tiles per wave for down).  Buckets larger than
-// 16 * TMAX tokens take several passes over the same weight rows.  Up to 16
-// tokens one token tile is held, and the row tiles per wave are the most
-// (gate-up 2, down 4) that still give every compute unit a workgroup: with
-// one or two activated experts (a draft step, or B = 1) fewer rows per
-// workgroup spread the weight stream over the whole GPU.
-#ifndef S2MOE_Q4_MEDIUM
-#define S2MOE_Q4_MEDIUM 2, 1, 2
-#endif
-#ifndef S2MOE_Q4_LARGE
-#define S2MOE_Q4_LARGE 2, 2, 4
-#endif
-
-template <int TMAX, int RG, int RD>
-hipError_t launch_q4_pair(const FfnArgs& a, hipStream_t s) {
-  hipError_t err = launch_q4_mode<0, TMAX, RG>(a, s);
-  return err != hipSuccess ? err : launch_q4_mode<1, TMAX, RD>(a, s);
-}
-
 // Compute units of the current device, queried once per device.
 hipError_t device_cus(int* cus) {
   static std::atomic<int> cache[64];
@@ -372,7 +565,29 @@ hipError_t device_cus(int* cus) {
   return hipSuccess;
 }
 
-hipError_t launch_q4_small(const FfnArgs& a, hipStream_t s) {
+template <int kMode, int R, int W>
+hipError_t launch_q4_rows(const FfnArgs& a, hipStream_t s) {
+  const dim3 grid(n_blocks(a, kMode, 16 * R * W));
+  if (a.packed)
+    hipLaunchKernelGGL((ffn_q4_rows_kernel<kMode, R, W, true>), grid, dim3(W * 64), 0, s, a);
+  else
+    hipLaunchKernelGGL((ffn_q4_rows_kernel<kMode, R, W, false>), grid, dim3(W * 64), 0, s, a);
+  return hipGetLastError();
+}
+
+// Tile choices per batch size.  Up to 16 tokens one token tile is held, and
+// the row tiles per wave are the most (gate-up 2, down 4) that still give
+// every compute unit a workgroup: with one or two activated experts (a draft
+// step, or B = 1) fewer rows per workgroup spread the weight stream over the
+// whole GPU.  Above 16 tokens gate-up runs on the row-split kernel (two
+// token tiles, activations shared through LDS) and down holds two token
+// tiles with 4 row tiles per wave.  Buckets larger than 32 tokens take
+// several passes over the same weight rows.
+hipError_t launch_q4_tiles(const FfnArgs& a, hipStream_t s) {
+  if (a.B > 16) {
+    const hipError_t err = launch_q4_rows<0, 2, 4>(a, s);
+    return err != hipSuccess ? err : launch_q4_mode<1, 2, 4>(a, s);
+  }
   int cus = 0;
   hipError_t err = device_cus(&cus);
   if (err != hipSuccess) return err;
@@ -389,11 +604,8 @@ hipError_t launch_ffn_q4(const FfnArgs& a, hipStream_t s) {
   const int n8 = a.B * a.H / 8;
   hipLaunchKernelGGL(q4_prep_x_kernel, dim3((n8 + 255) / 256), dim3(256), 0, s,
                      static_cast<const uint16_t*>(a.x), static_cast<uint16_t*>(a.x16), n8);
-  hipError_t err = hipGetLastError();
-  if (err != hipSuccess) return err;
-  if (a.B <= 16) return launch_q4_small(a, s);
-  if (a.B <= 32) return launch_q4_pair<S2MOE_Q4_MEDIUM>(a, s);
-  return launch_q4_pair<S2MOE_Q4_LARGE>(a, s);
+  const hipError_t err = hipGetLastError();
+  return err != hipSuccess ? err : launch_q4_tiles(a, s);
 }
 
 }  // namespace s2moe

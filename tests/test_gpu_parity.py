@@ -140,6 +140,34 @@ def test_int4_deepseek_shaped_with_shared():
         check_outputs(got, ref, "q4g32", f"int4 F=1408 B={B}")
 
 
+@pytest.mark.parametrize("hidden,B,seed", [(384, 48, 71), (640, 40, 62), (512, 64, 63)])
+def test_int4_row_split_gate_up(hidden, B, seed):
+    """Above 16 tokens the int4 gate-up runs on the row-split kernel with
+    LDS-staged activations: hidden sizes of 3, 5 and 4 super-steps (an odd
+    count ends on a half chunk), buckets of up to 16, 17-32 and more than 32
+    tokens (two passes over the rows), a shared expert in one case; packed
+    equal to row-major bit for bit, outputs against the oracle."""
+    S = 1 if hidden == 640 else 0
+    shape = LayerShape(hidden=hidden, ffn=256, n_experts=8, top_k=2, cap=4, alpha=0.5,
+                       n_shared=S, ffn_shared=128 if S else 0, act="bf16", wdt="q4g32")
+    d = make_inputs(shape, B, seed=seed, rho=0.6)
+    label = f"int4 row-split H={hidden} B={B}"
+    log(f"[parity] {label}")
+    got, _ = run_gpu(shape, d)
+    packed, _ = run_gpu(shape, d, packed=True)
+    counts = np.asarray(got["count"])
+    assert counts.max() > 32 and ((counts > 16) & (counts <= 32)).any(), counts
+    assert np.array_equal(packed["expert_out"], got["expert_out"]), label
+    assert np.array_equal(packed["y"], got["y"]), label
+    deq = lambda ex: {n: np.stack([oracle.dequant_q4g32(ex[n][e], ex[n + "_s"][e])  # noqa: E731
+                                   for e in range(ex[n].shape[0])]).astype(np.float32)
+                      for n in ("gate", "up", "down")} if ex else {}
+    ref = oracle.forward(d["x"], d["router"], d["conf_w"], deq(d["experts"]), deq(d["shared"]),
+                         shape.with_(wdt="f32"))
+    check_routing(got, ref, label)
+    check_outputs(got, ref, "q4g32", label)
+
+
 def test_max_hidden():
     """H = 16384 (the documented maximum): long router rows and gate-up
     rows, bf16, small B."""
