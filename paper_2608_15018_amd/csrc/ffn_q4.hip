@@ -19,7 +19,7 @@
 //
 // Work decomposition as in the bf16 kernel: R 16-row tiles per unit, W waves
 // split K, two-stage register pipeline, LDS reduction in wave order.  Above
-// 16 tokens the gate-up launch instead uses a row-split kernel whose waves
+// 8 tokens the gate-up launch instead uses a row-split kernel whose waves
 // share LDS-staged activations (ffn_q4_rows_kernel).
 #include <atomic>
 
@@ -286,12 +286,12 @@ __global__ __launch_bounds__(W * 64) void ffn_q4_kernel(FfnArgs a) {
   }
 }
 
-// Row-split variant for two token tiles: the W = 4 waves of a workgroup take
-// different row tiles over all of K, and share the activations, which the
-// workgroup stages in LDS two super-steps at a time (double-buffered, one
-// barrier per two super-steps).  The B operands then come from LDS instead
-// of one global load per wave, which at two token tiles would move twice the
-// weight bytes through the texture units.
+// Row-split variant (one or two token tiles per pass): the W waves of a
+// workgroup take different row tiles over all of K, and share the
+// activations, which the workgroup stages in LDS two super-steps at a time
+// (double-buffered, one barrier per two super-steps).  The B operands then
+// come from LDS instead of one global load per wave, which at two token
+// tiles would move twice the weight bytes through the texture units.
 constexpr int kChunkU4 = 32;       // u32x4 of one token row per chunk (2 super-steps)
 constexpr int kLdsRowU4 = kChunkU4 + 1;  // padded: the 16 rows of a tile hit distinct banks
 
@@ -575,24 +575,32 @@ hipError_t launch_q4_rows(const FfnArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-// Tile choices per batch size.  Up to 16 tokens one token tile is held, and
-// the row tiles per wave are the most (gate-up 2, down 4) that still give
-// every compute unit a workgroup: with one or two activated experts (a draft
-// step, or B = 1) fewer rows per workgroup spread the weight stream over the
-// whole GPU.  Above 16 tokens gate-up runs on the row-split kernel (two
-// token tiles, activations shared through LDS) and down holds two token
-// tiles with 4 row tiles per wave.  Buckets larger than 32 tokens take
-// several passes over the same weight rows.
+// Tile choices per batch size.
+// - Gate-up above 8 tokens runs on the row-split kernel with one row tile
+//   per wave (64 rows per workgroup, activations shared through LDS, up to
+//   two token tiles per pass).  One row tile per wave keeps it at three
+//   waves per SIMD (two row tiles: two), and the finer work units leave a
+//   smaller partly filled last round of workgroups.
+// - Gate-up up to 8 tokens and down up to 16 tokens hold one token tile,
+//   and the row tiles per wave are the most (gate-up 2, down 4) that still
+//   give every compute unit a workgroup: with one or two activated experts
+//   (a draft step, or B = 1) fewer rows per workgroup spread the weight
+//   stream over the whole GPU.
+// - Down above 16 tokens holds two token tiles with 4 row tiles per wave.
+//   Buckets larger than 32 tokens take several passes over the same rows.
 hipError_t launch_q4_tiles(const FfnArgs& a, hipStream_t s) {
-  if (a.B > 16) {
-    const hipError_t err = launch_q4_rows<0, 2, 4>(a, s);
-    return err != hipSuccess ? err : launch_q4_mode<1, 2, 4>(a, s);
-  }
+  hipError_t err;
   int cus = 0;
-  hipError_t err = device_cus(&cus);
+  if (a.B > 8) {
+    err = launch_q4_rows<0, 1, 4>(a, s);
+  } else {
+    err = device_cus(&cus);
+    if (err != hipSuccess) return err;
+    err = n_blocks(a, 0, 32) >= cus ? launch_q4_mode<0, 1, 2>(a, s) : launch_q4_mode<0, 1, 1>(a, s);
+  }
   if (err != hipSuccess) return err;
-  err = n_blocks(a, 0, 32) >= cus ? launch_q4_mode<0, 1, 2>(a, s) : launch_q4_mode<0, 1, 1>(a, s);
-  if (err != hipSuccess) return err;
+  if (a.B > 16) return launch_q4_mode<1, 2, 4>(a, s);
+  if (cus == 0 && (err = device_cus(&cus)) != hipSuccess) return err;
   if (n_blocks(a, 1, 64) >= cus) return launch_q4_mode<1, 1, 4>(a, s);
   if (n_blocks(a, 1, 32) >= cus) return launch_q4_mode<1, 1, 2>(a, s);
   return launch_q4_mode<1, 1, 1>(a, s);
