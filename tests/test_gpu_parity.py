@@ -74,7 +74,7 @@ def test_alpha_sweep_small(alpha):
         np.testing.assert_array_equal(got["idx"], got["plain_idx"])
 
 
-@pytest.mark.parametrize("B", [1, 4, 16, 64])
+@pytest.mark.parametrize("B", [1, 4, 8, 12, 16, 64])
 def test_int4_draft_sizes_small(B):
     shape = SMALL["c5s"][0]
     d = make_inputs(shape, B, seed=300 + B, rho=0.6)
