@@ -390,6 +390,121 @@ def layer_shape_of(m: dict, wdt: str):
                       act="bf16", wdt=wdt)
 
 
+def bench_stack(args, wl, shape, B: int, wid: int) -> int:
+    """`--layers L` layers of a verify-MoE workload run back to back, each with
+    its own router, hidden states and confidences (the host generator, per
+    layer) and its own expert weights (drawn on the device: the 24-layer int4
+    stack holds 19 GB), all packed.  A step is one full pass (route, gate,
+    experts, combine) through every layer; the FFN roofline covers the expert
+    launches of all layers, which stream far more than the caches hold."""
+    import torch
+
+    import paper_2608_15018_amd as s2
+    from synth import device_gen, gen
+
+    L = args.layers
+    if L > wl.n_layers:
+        raise SystemExit(f"{wl.name} has {wl.n_layers} layer(s)")
+    E, F, H, S, Fs = shape.n_experts, shape.ffn, shape.hidden, shape.n_shared, shape.ffn_shared
+    layer = s2.make_layer(shape, flags=shape.flags | s2.PACKED_WEIGHTS)
+    t0 = time.time()
+    keep, passes, ins = [], [], []
+    for l in range(L):
+        router = gen.make_router(shape, args.seed, l, wid, wl.router_std)
+        x, conf_w, _ = gen.make_batch(shape, B, args.seed, l, wid, wl.rho)
+        ex = device_gen.expert_weights(E, F, H, shape.wdt, args.seed, l, std=wl.w_std)
+        sh = device_gen.expert_weights(S, Fs, H, shape.wdt, args.seed, l, tag=1,
+                                       std=wl.w_std) if S else {}
+        dev, w = s2.pack_expert_weights((ex, sh), shape.wdt)
+        del ex, sh
+        keep.append(dev)
+        passes.append(s2.VerifyPass(layer, B))
+        ins.append((s2.to_device(x), s2.to_device(router), s2.to_device(conf_w), w))
+    torch.cuda.synchronize()
+    _log(f"[bench] {wl.name}: {L} layers generated and packed in {time.time() - t0:.1f}s")
+
+    def step():
+        for p, (x, r, c, w) in zip(passes, ins):
+            p(x, r, c, w)
+
+    for _ in range(max(1, args.warmup)):
+        step()
+    torch.cuda.synchronize()
+    n_uniq = [int(p.rt.n_uniq.item()) for p in passes]
+    nbytes = sum(n_uniq) * expert_bytes(shape, F) + L * S * expert_bytes(shape, Fs)
+
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t_start
+
+    # The expert launches alone: every layer's s2moe_verify_moe, back to back,
+    # between one pair of HIP events on the launch stream.
+    stream = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    _head_start()
+    e0.record(stream)
+    for _ in range(args.steps):
+        for p, (x, _r, _c, w) in zip(passes, ins):
+            p.verify_moe(x, w)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ffn_s = e0.elapsed_time(e1) / 1e3 / args.steps  # per pass through the L layers
+    achieved = nbytes / ffn_s / 1e9
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+        router = gen.make_router(shape, args.seed, 0, wid, wl.router_std)
+        x, conf_w, _ = gen.make_batch(shape, B, args.seed, 0, wid, wl.rho)
+        experts = gen.make_experts(shape, args.seed, 0, wid, wl.w_std)
+        shared = gen.make_shared_experts(shape, args.seed, 0, wid, wl.w_std)
+        t = time.perf_counter()
+        oracle.forward(x, router, conf_w, experts, shared, shape)
+        dt = time.perf_counter() - t
+        try:
+            from threadpoolctl import threadpool_info
+            cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+        except Exception:  # pragma: no cover
+            cores = os.cpu_count()
+        cpu = {"value": B / (dt * L), "unit": "draft tokens/s", "cores": cores, "kind": "oracle",
+               "sample": f"one layer (layer 0, B={B}) of the {L}-layer stack, fp64 numpy, "
+                         f"{dt:.1f}s, scaled by {L} layers"}
+
+    out = {
+        "metric": "verify-MoE layer: draft tokens/s and achieved HBM GB/s (% of peak) on "
+                  "unique experts",
+        "value": B * args.steps / elapsed,
+        "unit": "draft tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": elapsed / args.steps * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": {"bf16": "bf16", "f32": "f32", "q4g32": "int4-g32/bf16"}[shape.wdt],
+        "data": "synthetic",
+        "config": {"workload": wl.description + f" ({L} layers, each its own inputs and weights)",
+                   "name": wl.name, "draft_tokens": B, "layers": L,
+                   "hidden": H, "ffn": F, "experts": E, "top_k": shape.top_k, "shared": S,
+                   "cap": shape.cap, "alpha": shape.alpha, "weights": "packed"},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "kernel": f"s2moe_verify_moe (expert gate-up + down launches, {L} layers)",
+                     "bytes_per_launch": nbytes / L, "avg_launch_us": ffn_s / L * 1e6},
+        "cpu_baseline": cpu,
+        "n_uniq_per_layer": n_uniq,
+        "ffn_timing": f"one event pair around {args.steps} passes through the {L} layers",
+        "ms_per_layer": elapsed / args.steps / L * 1e3,
+    }
+    print(json.dumps(out), flush=True)
+    return 0
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -407,6 +522,9 @@ def main(argv=None):
     ap.add_argument("--batch", type=int, default=None, help="draft tokens (default: workload's)")
     ap.add_argument("--alpha", type=float, default=None)
     ap.add_argument("--seed", type=int, default=1)
+    ap.add_argument("--layers", type=int, default=1,
+                    help="c*: verify this many layers of the workload back to back, each with its "
+                         "own router, hidden states, confidences and expert weights (c5: up to 24)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--plain-weights", action="store_true",
                     help="stream the row-major weights instead of the packed tile order")
@@ -450,6 +568,8 @@ def main(argv=None):
     default_B = wl.batches[-1 if args.workload == "c5" else 0]
     B = args.batch or default_B
     wid = WORKLOAD_ID[wl.name]
+    if args.layers > 1:
+        return bench_stack(args, wl, shape, B, wid)
 
     t0 = time.time()
     router = gen.make_router(shape, args.seed, 0, wid, wl.router_std)
@@ -560,7 +680,8 @@ def main(argv=None):
         "vs_baseline": None,
         "dtype": {"bf16": "bf16", "f32": "f32", "q4g32": "int4-g32/bf16"}[shape.wdt],
         "data": "synthetic",
-        "config": {"workload": wl.description, "name": wl.name, "draft_tokens": B,
+        "config": {"workload": wl.description + (" (one layer: layer 0)" if wl.n_layers > 1 else ""),
+                   "name": wl.name, "draft_tokens": B, "layers": 1,
                    "hidden": shape.hidden, "ffn": shape.ffn, "experts": shape.n_experts,
                    "top_k": shape.top_k, "shared": shape.n_shared, "cap": shape.cap,
                    "alpha": shape.alpha, "weights": "packed" if packed else "row-major"},
