@@ -95,6 +95,22 @@ def test_single_token():
     np.testing.assert_array_equal(got["idx"], got["plain_idx"])
 
 
+@pytest.mark.parametrize("B,E,k,cap,H,F,S,wdt", [
+    (13, 7, 3, 5, 320, 192, 0, "bf16"),
+    (37, 25, 4, 9, 192, 320, 1, "bf16"),
+    (5, 11, 2, 4, 384, 256, 0, "q4g32"),
+    (23, 13, 3, 6, 256, 384, 1, "q4g32"),
+])
+def test_odd_expert_counts_and_batches(B, E, k, cap, H, F, S, wdt):
+    """Expert counts that fill no 4- or 16-expert group, batch sizes that
+    fill no token tile, and (with S = 1) a shared expert of another width:
+    the routing kernels' partial expert groups and the FFN tails."""
+    shape = LayerShape(hidden=H, ffn=F, n_experts=E, top_k=k, cap=cap, alpha=0.5,
+                       n_shared=S, ffn_shared=F + 128 if S else 0, wdt=wdt)
+    d = make_inputs(shape, B, seed=900 + B, rho=0.5)
+    _full_check(shape, d, f"odd B={B} E={E} k={k} {wdt}")
+
+
 def test_max_tokens_one_hot_expert_load():
     """B = 256 (the ABI maximum) with strongly shared routing, so single
     experts receive far more than 64 tokens (several token passes)."""
