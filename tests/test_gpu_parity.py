@@ -111,6 +111,22 @@ def test_odd_expert_counts_and_batches(B, E, k, cap, H, F, S, wdt):
     _full_check(shape, d, f"odd B={B} E={E} k={k} {wdt}")
 
 
+@pytest.mark.parametrize("B", [1, 2, 4])
+@pytest.mark.parametrize("alpha", [0.0, 0.7])
+@pytest.mark.parametrize("flags", [0, 1, 2, 4, 7])
+@pytest.mark.parametrize("E,k,cap", [(8, 2, 4), (64, 6, 16), (200, 8, 20)])
+def test_small_batch_gating(B, alpha, flags, E, k, cap):
+    """Draft-sized batches (the single-wave gating path when alpha = 0 or
+    B = 1): every routing output against the oracle, for each reading of
+    the gating and expert counts in all three per-lane slot widths."""
+    shape = LayerShape(hidden=256, ffn=128, n_experts=E, top_k=k, cap=cap, alpha=alpha,
+                       flags=flags)
+    d = make_inputs(shape, B, seed=1000 + 7 * B + E + flags, rho=0.5)
+    got, ref = _full_check(shape, d, f"small B={B} alpha={alpha} flags={flags} E={E}")
+    if alpha == 0.0 or B == 1:
+        np.testing.assert_array_equal(got["idx"], got["plain_idx"])
+
+
 def test_max_tokens_one_hot_expert_load():
     """B = 256 (the ABI maximum) with strongly shared routing, so single
     experts receive far more than 64 tokens (several token passes)."""
