@@ -5,8 +5,9 @@
 // slice of H per item (H is sliced when there are few experts, so that all
 // waves load at once); its lanes split the slice in 16-byte chunks (the
 // token row and 4 router rows read coalesced, all in flight together), DPP
-// reductions add the lane partials and the slices are summed in order.  The workgroup then ranks the E logits (each
-// rank counted by several threads) and wave 0 lists the plain top-k.
+// reductions add the lane partials and the slices are summed in order.
+// Wave 0 then ranks the E logits: an exact top-(k+1) by ballots over the
+// order keys, as in the gating kernel.
 #include "kernels.h"
 #include "select.h"
 
@@ -65,34 +66,6 @@ __host__ __device__ inline int route_slices(int E, int chunks) {
   return S;
 }
 
-// Plain top-k and gap of token b from its E logits in ell_s (rank_s
-// zeroed and every thread past a barrier): rank every logit (value desc,
-// expert id asc), take ranks 0..k-1 in id order, gap = rank 0 - rank k.
-__device__ void select_plain(const RouteArgs& a, int b, const float* ell_s, int* rank_s,
-                             float* top1_s, float* kth1_s) {
-  const int tid = threadIdx.x, lane = tid & (kWave - 1), E = a.E, k = a.k;
-  block_rank_desc(ell_s, E, rank_s, tid, blockDim.x);
-  __syncthreads();
-  if (tid < E) {
-    if (rank_s[tid] == 0) *top1_s = ell_s[tid];
-    if (rank_s[tid] == k) *kth1_s = ell_s[tid];
-  }
-  __syncthreads();
-  if (wave_id() != 0) return;
-  uint32_t bits = 0;
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int e = lane + kWave * j;
-    if (e < E && rank_s[e] < k) bits |= 1u << j;
-  }
-  int rank[4];
-  wave_rank_flagged<4>(bits, rank);
-#pragma unroll
-  for (int j = 0; j < 4; ++j)
-    if ((bits >> j) & 1u) a.plain_idx[(size_t)b * k + rank[j]] = lane + kWave * j;
-  if (lane == 0) a.gap[b] = *top1_s - *kth1_s;
-}
-
 // Small batches: one wave per router row computes that expert's logit for
 // every token, so the E rows are streamed by E waves spread over the GPU
 // instead of by one workgroup per token.  Lanes take 16-byte chunks of H;
@@ -115,26 +88,58 @@ __global__ __launch_bounds__(256) void route_rows_kernel(RouteArgs a) {
   }
 }
 
-// Plain top-k and gap of each token from the logits route_rows_kernel wrote.
-__global__ __launch_bounds__(256) void route_select_kernel(RouteArgs a) {
-  __shared__ float ell_s[kMaxExperts];
-  __shared__ int rank_s[kMaxExperts];
-  __shared__ float top1_s, kth1_s;
-  const int b = blockIdx.x, tid = threadIdx.x;
-  if (tid < a.E) {
-    ell_s[tid] = a.logits[(size_t)b * a.E + tid];
-    rank_s[tid] = 0;
+// Plain top-k and gap of token b by one wave, from its E logits ell (LDS or
+// global): the exact top-(k+1) by (value desc, id asc); its last member
+// (smallest value, then largest id) is the (k+1)-th, the other k are the
+// plain top-k, listed in id order; gap = ell_(1) - ell_(k+1).
+template <int NJ>
+__device__ __forceinline__ void wave_select_plain(const RouteArgs& a, int b, const float* ell) {
+  const int lane = threadIdx.x & (kWave - 1), E = a.E, k = a.k;
+  uint32_t key[1][NJ];
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) {
+    const int e = lane + kWave * j;
+    key[0][j] = e < E ? order_key(ell[e]) : 0u;
   }
-  __syncthreads();
-  select_plain(a, b, ell_s, rank_s, &top1_s, &kth1_s);
+  uint32_t sel[1];
+  wave_top_k<1, NJ>(key, k + 1, sel);
+  uint32_t mn = 0xFFFFFFFFu, mx = 0u;
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) {
+    if ((sel[0] >> j) & 1u) mn = min(mn, key[0][j]);
+    mx = max(mx, key[0][j]);
+  }
+  mn = ~wave_max_key_dpp(~mn);
+  mx = wave_max_key_dpp(mx);
+  int last = -1;
+#pragma unroll
+  for (int j = NJ - 1; j >= 0; --j) {
+    const uint64_t m = __ballot(((sel[0] >> j) & 1u) && key[0][j] == mn);
+    if (last < 0 && m) last = kWave * j + 63 - __builtin_clzll(m);
+  }
+  uint32_t bits = 0;
+#pragma unroll
+  for (int j = 0; j < NJ; ++j)
+    if (((sel[0] >> j) & 1u) && lane + kWave * j != last) bits |= 1u << j;
+  int rank[NJ];
+  wave_rank_flagged<NJ>(bits, rank);
+#pragma unroll
+  for (int j = 0; j < NJ; ++j)
+    if ((bits >> j) & 1u) a.plain_idx[(size_t)b * k + rank[j]] = lane + kWave * j;
+  if (lane == 0) a.gap[b] = key_value(mx) - key_value(mn);
 }
 
-template <bool kBf16>
+// Small batches, second launch: one wave per token ranks the logits
+// route_rows_kernel wrote.
+template <int NJ>
+__global__ __launch_bounds__(kWave) void route_select_wave_kernel(RouteArgs a) {
+  wave_select_plain<NJ>(a, blockIdx.x, a.logits + (size_t)blockIdx.x * a.E);
+}
+
+template <bool kBf16, int NJ>
 __global__ __launch_bounds__(1024) void route_kernel(RouteArgs a) {
   __shared__ float part_s[kMaxExperts];  // [slice][E]: slices * E <= 256
   __shared__ float ell_s[kMaxExperts];
-  __shared__ int rank_s[kMaxExperts];
-  __shared__ float top1_s, kth1_s;
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
   const int wave = wave_id();
@@ -148,7 +153,6 @@ __global__ __launch_bounds__(1024) void route_kernel(RouteArgs a) {
   const int S = route_slices(E, chunks);
   const int per_slice = (chunks + S - 1) / S;
 
-  if (tid < E) rank_s[tid] = 0;
   // Work item p = (slice, group of 4 experts), p = slice * groups + group.
   for (int p = wave; p < S * groups; p += n_waves) {
     const int slice = p / groups, e0 = (p - slice * groups) * 4;
@@ -169,7 +173,7 @@ __global__ __launch_bounds__(1024) void route_kernel(RouteArgs a) {
     a.logits[(size_t)b * E + tid] = v;
   }
   __syncthreads();
-  select_plain(a, b, ell_s, rank_s, &top1_s, &kth1_s);
+  if (wave == 0) wave_select_plain<NJ>(a, b, ell_s);
 }
 
 }  // namespace
@@ -189,18 +193,29 @@ hipError_t launch_route(const RouteArgs& a, hipStream_t s) {
       hipLaunchKernelGGL(route_rows_kernel<false>, grid, dim3(256), 0, s, a);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(route_select_kernel, dim3(a.B), dim3(256), 0, s, a);
+    if (a.E <= 64)
+      hipLaunchKernelGGL(route_select_wave_kernel<1>, dim3(a.B), dim3(kWave), 0, s, a);
+    else if (a.E <= 128)
+      hipLaunchKernelGGL(route_select_wave_kernel<2>, dim3(a.B), dim3(kWave), 0, s, a);
+    else
+      hipLaunchKernelGGL(route_select_wave_kernel<4>, dim3(a.B), dim3(kWave), 0, s, a);
     return hipGetLastError();
   }
-  // One wave per (H slice, 4 experts) item, at most 16; E <= 256 keeps at
-  // least one thread per expert for the ranking.
+  // One wave per (H slice, 4 experts) item, at most 16; with 4 experts per
+  // wave there is a thread per expert to add the slices.
   const int chunks = a.H / (a.bf16 ? 8 : 4);
   const int waves = min(16, route_slices(a.E, chunks) * ((a.E + 3) / 4));
   const dim3 block(64 * waves);
-  if (a.bf16)
-    hipLaunchKernelGGL(route_kernel<true>, dim3(a.B), block, 0, s, a);
-  else
-    hipLaunchKernelGGL(route_kernel<false>, dim3(a.B), block, 0, s, a);
+  if (a.E <= 64) {
+    if (a.bf16) hipLaunchKernelGGL((route_kernel<true, 1>), dim3(a.B), block, 0, s, a);
+    else hipLaunchKernelGGL((route_kernel<false, 1>), dim3(a.B), block, 0, s, a);
+  } else if (a.E <= 128) {
+    if (a.bf16) hipLaunchKernelGGL((route_kernel<true, 2>), dim3(a.B), block, 0, s, a);
+    else hipLaunchKernelGGL((route_kernel<false, 2>), dim3(a.B), block, 0, s, a);
+  } else {
+    if (a.bf16) hipLaunchKernelGGL((route_kernel<true, 4>), dim3(a.B), block, 0, s, a);
+    else hipLaunchKernelGGL((route_kernel<false, 4>), dim3(a.B), block, 0, s, a);
+  }
   return hipGetLastError();
 }
 
