@@ -274,13 +274,22 @@ __global__ __launch_bounds__(kWave) void reuse_gate_small_kernel(GateArgs a) {
   const int lane = threadIdx.x;
   const int B = a.B, E = a.E, k = a.k, n_asg = B * k;
 
-  float w[kSmallMaxTokens];
+  // Every global read is issued up front: confidences, gaps, the plain top-k
+  // and all B x E logits (at most 4 x 4 per lane).
+  float w[kSmallMaxTokens], gap[kSmallMaxTokens], lg[kSmallMaxTokens][kNJ];
   int active = 0;
 #pragma unroll
   for (int b = 0; b < kSmallMaxTokens; ++b) {
     w[b] = b < B ? fmaxf(a.conf_w[b], 0.f) : 0.f;
+    gap[b] = b < B ? a.gap[b] : 0.f;
+#pragma unroll
+    for (int j = 0; j < kNJ; ++j) {
+      const int e = lane + kWave * j;
+      lg[b][j] = b < B && e < E ? a.logits[(size_t)b * E + e] : 0.f;
+    }
     active |= w[b] > 0.f;
   }
+  const int pidx = lane < n_asg ? a.plain_idx[lane] : 0;
   const bool activated_only = (a.flags & kPrefActivatedOnly) != 0;
 #pragma unroll
   for (int j = 0; j < kMaxExperts / kWave; ++j) {
@@ -292,7 +301,7 @@ __global__ __launch_bounds__(kWave) void reuse_gate_small_kernel(GateArgs a) {
   // nothing is addressed out of range.
   int my_e = 0;
   if (lane < n_asg) {
-    my_e = min(max(a.plain_idx[lane], 0), E - 1);
+    my_e = min(max(pidx, 0), E - 1);
     idx_s[lane] = my_e;
   }
   __syncthreads();
@@ -316,8 +325,9 @@ __global__ __launch_bounds__(kWave) void reuse_gate_small_kernel(GateArgs a) {
       float tot = 0.f;
       for (int part = 0; part < parts; ++part) {
         float sum = 0.f;
-        for (int b = part * run; b < min(B, part * run + run); ++b)
-          sum = fmaf(w[b], a.logits[(size_t)b * E + e], sum);
+#pragma unroll
+        for (int b = 0; b < kSmallMaxTokens; ++b)
+          if (b >= part * run && b < min(B, part * run + run)) sum = fmaf(w[b], lg[b][j], sum);
         tot = part == 0 ? sum : tot + sum;
       }
       a.g[e] = tot;
@@ -346,16 +356,15 @@ __global__ __launch_bounds__(kWave) void reuse_gate_small_kernel(GateArgs a) {
 
   // Per token: the plain top-k and its gate weights.
   const bool from_biased = (a.flags & kGateFromBiased) != 0;
-  for (int b = 0; b < B; ++b) {
-    const float lam = active ? ((a.flags & kBiasAbsolute) ? a.alpha : a.alpha * a.gap[b]) : 0.f;
-    uint32_t bits = 0;
-    float l[kNJ], x[kNJ];
 #pragma unroll
-    for (int j = 0; j < kNJ; ++j) {
-      const int e = lane + kWave * j;
-      l[j] = e < E ? a.logits[(size_t)b * E + e] : 0.f;
-      x[j] = from_biased && ((pref_bits >> j) & 1u) ? l[j] + lam : l[j];
-    }
+  for (int b = 0; b < kSmallMaxTokens; ++b) {
+    if (b >= B) break;
+    const float lam = active ? ((a.flags & kBiasAbsolute) ? a.alpha : a.alpha * gap[b]) : 0.f;
+    uint32_t bits = 0;
+    float x[kNJ];
+#pragma unroll
+    for (int j = 0; j < kNJ; ++j)
+      x[j] = from_biased && ((pref_bits >> j) & 1u) ? lg[b][j] + lam : lg[b][j];
     for (int q = 0; q < k; ++q) {
       const int e = idx_s[b * k + q];
       if ((e & (kWave - 1)) == lane) bits |= 1u << (e / kWave);
