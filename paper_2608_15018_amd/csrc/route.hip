@@ -1,7 +1,10 @@
 // Router logits and plain top-(k+1) per draft token (Sec. "Reuse-aware
 // Expert Gating": target gating logits ell_b; gap_b = ell_(1) - ell_(k+1)).
 //
-// One workgroup of up to 16 waves per token.  A wave takes 4 experts and a
+// Two paths.  Small batches, and batches over many experts, compute the
+// logits with one wave per (router row, token) pair and rank them in a second
+// launch, one wave per token.  Otherwise one workgroup of up to 16 waves per
+// token does both.  There a wave takes 4 experts and a
 // slice of H per item (H is sliced when there are few experts, so that all
 // waves load at once); its lanes split the slice in 16-byte chunks (the
 // token row and 4 router rows read coalesced, all in flight together), DPP
@@ -66,26 +69,25 @@ __host__ __device__ inline int route_slices(int E, int chunks) {
   return S;
 }
 
-// Small batches: one wave per router row computes that expert's logit for
-// every token, so the E rows are streamed by E waves spread over the GPU
-// instead of by one workgroup per token.  Lanes take 16-byte chunks of H;
-// a DPP reduction adds them.
+// Small batches and many experts: one wave per (router row, token) pair
+// (grid: E / 4 x B workgroups of 4 waves), so the E rows are streamed by
+// waves spread over the GPU instead of by one workgroup per token.  Lanes
+// take 16-byte chunks of H; a DPP reduction adds them.
 template <bool kBf16>
 __global__ __launch_bounds__(256) void route_rows_kernel(RouteArgs a) {
   const int lane = threadIdx.x & (kWave - 1);
   const int e = blockIdx.x * 4 + wave_id();
+  const int b = blockIdx.y;
   if (e >= a.E) return;
   const size_t row = (size_t)a.H * (kBf16 ? 2 : 4);
   const u32x4* wr = reinterpret_cast<const u32x4*>(static_cast<const char*>(a.router) + e * row);
+  const u32x4* xr = reinterpret_cast<const u32x4*>(static_cast<const char*>(a.x) + b * row);
   const int chunks = a.H / (kBf16 ? 8 : 4);
-  for (int b = 0; b < a.B; ++b) {
-    const u32x4* xr = reinterpret_cast<const u32x4*>(static_cast<const char*>(a.x) + b * row);
-    float acc = 0.f;
+  float acc = 0.f;
 #pragma unroll 4
-    for (int c = lane; c < chunks; c += kWave) acc = dot_chunk<kBf16>(xr[c], wr[c], acc);
-    acc = wave_sum_dpp(acc);
-    if (lane == 0) a.logits[(size_t)b * a.E + e] = acc;
-  }
+  for (int c = lane; c < chunks; c += kWave) acc = dot_chunk<kBf16>(xr[c], wr[c], acc);
+  acc = wave_sum_dpp(acc);
+  if (lane == 0) a.logits[(size_t)b * a.E + e] = acc;
 }
 
 // Plain top-k and gap of token b by one wave, from its E logits ell (LDS or
@@ -178,15 +180,21 @@ __global__ __launch_bounds__(1024) void route_kernel(RouteArgs a) {
 
 }  // namespace
 
-// Below this many tokens the router rows are spread over the GPU (two
-// launches) instead of one workgroup per token.
+// The two-launch path (router rows spread over the GPU, then one wave per
+// token ranking its logits) serves batches up to this many tokens, and every
+// batch when there are more than S2MOE_ROUTE_ROWS_MIN_E experts (the one
+// workgroup per token of route_kernel would stream the whole router through
+// each token's compute unit).
 #ifndef S2MOE_ROUTE_ROWS_MAX_B
 #define S2MOE_ROUTE_ROWS_MAX_B 8
 #endif
+#ifndef S2MOE_ROUTE_ROWS_MIN_E
+#define S2MOE_ROUTE_ROWS_MIN_E 64
+#endif
 
 hipError_t launch_route(const RouteArgs& a, hipStream_t s) {
-  if (a.B <= S2MOE_ROUTE_ROWS_MAX_B) {
-    const dim3 grid((a.E + 3) / 4);
+  if (a.B <= S2MOE_ROUTE_ROWS_MAX_B || a.E > S2MOE_ROUTE_ROWS_MIN_E) {
+    const dim3 grid((a.E + 3) / 4, a.B);
     if (a.bf16)
       hipLaunchKernelGGL(route_rows_kernel<true>, grid, dim3(256), 0, s, a);
     else
