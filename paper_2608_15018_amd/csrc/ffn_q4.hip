@@ -578,7 +578,7 @@ hipError_t launch_q4_rows(const FfnArgs& a, hipStream_t s) {
 // Tile choices per batch size.
 // - Gate-up above 8 tokens runs on the row-split kernel with one row tile
 //   per wave (64 rows per workgroup, activations shared through LDS, up to
-//   two token tiles per pass).  One row tile per wave keeps it at three
+//   two token tiles per pass).  One row tile per wave keeps it at four
 //   waves per SIMD (two row tiles: two), and the finer work units leave a
 //   smaller partly filled last round of workgroups.
 // - Gate-up up to 8 tokens and down up to 16 tokens hold one token tile,
