@@ -36,7 +36,7 @@ HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
 # The oracle baselines repeat their sample until about this many seconds of
 # host work have passed (at least once, at most ORACLE_MAX_REPS times).
 ORACLE_MIN_S = 10.0
-ORACLE_MAX_REPS = 50
+ORACLE_MAX_REPS = 1000
 
 
 def time_oracle(fn) -> tuple[int, float]:
