@@ -111,6 +111,22 @@ def test_odd_expert_counts_and_batches(B, E, k, cap, H, F, S, wdt):
     _full_check(shape, d, f"odd B={B} E={E} k={k} {wdt}")
 
 
+@pytest.mark.parametrize("B,E,k,cap,act", [
+    (24, 96, 4, 8, "f32"),
+    (40, 130, 5, 10, "bf16"),
+    (9, 200, 8, 20, "f32"),
+])
+def test_router_rows_path_many_experts(B, E, k, cap, act):
+    """Batches over more than 64 experts take the two-launch router (one wave
+    per router row and token, then one wave per token ranking) at any B:
+    fp32 and bf16 activations, an expert count that fills no 4-expert group
+    (130) and one that needs four experts per lane in the ranking (200)."""
+    shape = LayerShape(hidden=256, ffn=128, n_experts=E, top_k=k, cap=cap, alpha=0.5,
+                       act=act, wdt=act)
+    d = make_inputs(shape, B, seed=1300 + B, rho=0.5)
+    _full_check(shape, d, f"router rows B={B} E={E} {act}")
+
+
 @pytest.mark.parametrize("B", [1, 2, 4])
 @pytest.mark.parametrize("alpha", [0.0, 0.7])
 @pytest.mark.parametrize("flags", [0, 1, 2, 4, 7])
