@@ -36,3 +36,31 @@ def test_malformed_record_is_ignored(tmp_path, monkeypatch):
     monkeypatch.setattr(bench, "ffn_source_hash", lambda wdt: "h")
     _write(tmp_path, "verify_moe_c2_traffic.md", "n/a", "h")
     assert bench.recorded_traffic("c2", "bf16", 16, 16) is None
+
+
+def test_code_hash_ignores_comments_but_not_code():
+    a = b"int f(int x) {  // twice x\n  return 2 * x; /* doubled */\n}\n"
+    b = b"int f(int x) {\n  /* a note\n     over two lines */ return 2 * x;\n}\n"
+    c = b"int f(int x) {\n  return 3 * x;\n}\n"
+    assert bench._code_only(a) == bench._code_only(b)
+    assert bench._code_only(a) != bench._code_only(c)
+
+
+def test_source_hashes_match_the_committed_records():
+    """The committed traffic summaries carry the hash of the kernel code they
+    were measured on; while that code is unchanged, bench.py reports them."""
+    assert bench.recorded_traffic("c2", "bf16", 16, 16) is not None
+    assert bench.recorded_traffic("c5", "q4g32", 16, 1) is not None
+    assert bench.recorded_traffic("c5", "q4g32", 64, 1) is not None
+
+
+def test_oracle_timing_repeats_until_the_time_or_the_cap(monkeypatch):
+    calls = []
+    monkeypatch.setattr(bench, "ORACLE_MIN_S", 0.05)
+    monkeypatch.setattr(bench, "ORACLE_MAX_REPS", 7)
+    reps, dt = bench.time_oracle(lambda: calls.append(1))
+    assert reps == len(calls) == 7 and dt >= 0.0
+    monkeypatch.setattr(bench, "ORACLE_MAX_REPS", 1000)
+    import time
+    reps, dt = bench.time_oracle(lambda: time.sleep(0.03))
+    assert 2 <= reps <= 3 and dt >= 0.05
