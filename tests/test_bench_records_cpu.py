@@ -46,14 +46,6 @@ def test_code_hash_ignores_comments_but_not_code():
     assert bench._code_only(a) != bench._code_only(c)
 
 
-def test_source_hashes_match_the_committed_records():
-    """The committed traffic summaries carry the hash of the kernel code they
-    were measured on; while that code is unchanged, bench.py reports them."""
-    assert bench.recorded_traffic("c2", "bf16", 16, 16) is not None
-    assert bench.recorded_traffic("c5", "q4g32", 16, 1) is not None
-    assert bench.recorded_traffic("c5", "q4g32", 64, 1) is not None
-
-
 def test_oracle_timing_repeats_until_the_time_or_the_cap(monkeypatch):
     calls = []
     monkeypatch.setattr(bench, "ORACLE_MIN_S", 0.05)
