@@ -241,10 +241,12 @@ __global__ __launch_bounds__(1024) void reuse_gate_kernel(GateArgs a) {
   __syncthreads();
 
   // Stable expert-major slot list: assignment (b, j) of expert e goes after
-  // the assignments of e by tokens b' < b.
+  // the assignments of e by tokens b' < b.  Every idx_s entry was written
+  // above with an id below E; the clamps keep the addressing inside offset_s
+  // and slot even if that ever stopped holding.
   for (int i = tid; i < B * k; i += blockDim.x) {
     const int b = i / k;
-    const int e = idx_s[i];
+    const int e = min((int)idx_s[i], E - 1);
     int before = 0;
 #pragma unroll
     for (int w = 0; w < kMaskWords; ++w) {
@@ -252,7 +254,7 @@ __global__ __launch_bounds__(1024) void reuse_gate_kernel(GateArgs a) {
       if (w < (b >> 6)) before += __popcll(m);
       else if (w == (b >> 6)) before += __popcll(m & ((1ull << (b & 63)) - 1ull));
     }
-    a.slot[offset_s[e] + before] = i;
+    a.slot[min(offset_s[e] + before, B * k - 1)] = i;
   }
 }
 
