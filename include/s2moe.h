@@ -60,14 +60,24 @@ typedef enum s2moe_dtype {
   /* weights only: 4-bit codes q in [0,15], two per byte (element 2i in the
      low nibble of byte i), value s * (q - 8) with one fp16 scale s per 32
      consecutive elements along K.  Codes [rows, K/2] u8, scales [rows, K/32]
-     f16, per expert. */
+     f16, per expert.
+     Range: with these weights the kernels compute in fp16 with fp32
+     accumulation.  x is converted from bf16 to fp16, each weight is rounded
+     once to fp16 as s * (q - 8), and the SwiGLU activations
+     silu(W_g x) * (W_u x) are stored in fp16.  Every |x|, |s * (q - 8)|
+     and activation must therefore stay below 65504 (larger finite values
+     become infinite, with no error), and magnitudes below about 6.1e-5
+     keep fewer significant bits (fp16 subnormals). */
   S2MOE_Q4G32 = 2
 } s2moe_dtype;
 
 /* Readings of the paper's gating where the text leaves a choice (0 = default). */
 enum {
-  /* TopCap candidates restricted to experts in some token's plain top-k
-     ("experts that already exhibit repeated activation"); |E*| <= cap. */
+  /* TopCap candidates restricted to experts that some token of the batch
+     already selects in its plain top-k, so that E* holds at most cap of
+     them (Sec. "Reuse-aware Expert Gating", opening paragraph and "Global
+     preferred expert selection": the preferred experts are read there as
+     ones the batch already activates).  Default: all E experts compete. */
   S2MOE_PREF_ACTIVATED_ONLY = 1u,
   /* lambda_b = alpha instead of alpha * gap_b. */
   S2MOE_BIAS_ABSOLUTE = 2u,
@@ -179,8 +189,14 @@ s2moe_status s2moe_pack_weights(int32_t w_dtype, int32_t n_mats, int32_t rows, i
                                 const void *src, const void *src_scales, void *dst,
                                 void *dst_scales, void *stream);
 
-/* Combine: y_b = sum_{j<k} gate_w[b,j] expert_out[b*k+j] +
-   sum_{s<S} expert_out[B*k + s*B + b], summed in that order (fp32). */
+/* Combine (MoE layer definition: each token's output is the gate-weighted
+   sum of its k routed experts' outputs plus, with weight 1, every shared
+   expert's output):
+   y_b = sum_{j<k} gate_w[b,j] expert_out[b*k+j] +
+   sum_{s<S} expert_out[B*k + s*B + b], summed in that order (fp32).
+   Reads r->gate_w [B, k] and expert_out [B*k + S*B, H] as written by
+   s2moe_reuse_gate and s2moe_verify_moe; writes y [B, H] fp32 (caller-owned,
+   must not overlap expert_out).  Errors as for every entry point. */
 s2moe_status s2moe_combine(const s2moe_layer *layer, int32_t n_tokens,
                            const s2moe_routing *r, const float *expert_out, float *y,
                            void *stream);

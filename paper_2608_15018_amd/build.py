@@ -1,6 +1,7 @@
 """Build libs2moe.so for gfx950 with hipcc (in-tree, no JIT cache).
 
-    python -m paper_2608_15018_amd.build
+    python -m paper_2608_15018_amd.build                   # the library
+    python -m paper_2608_15018_amd.build --host-sanitize   # + ASan/UBSan host layer
 """
 
 from __future__ import annotations
@@ -61,5 +62,55 @@ def build(verbose: bool = True, out: str = LIB, objdir: str = OBJDIR, defines=()
     return out
 
 
+# Host-side checking build: the C-ABI layer (argument validation, workspace
+# arithmetic, struct marshalling) compiled by g++ with AddressSanitizer and
+# UndefinedBehaviorSanitizer, linked with the regular device objects.  The
+# kernels are not instrumented (no device sanitizer is used).  Load it with
+# the ASan runtime first in LD_PRELOAD (host_sanitizer_env) and point
+# S2MOE_LIBRARY at it.
+SAN_LIB = os.path.join(OBJDIR, "libs2moe_hostsan.so")
+SAN_FLAGS = ["-fsanitize=address,undefined", "-fno-sanitize-recover=undefined",
+             "-fno-omit-frame-pointer"]
+
+
+def build_host_sanitized(verbose: bool = True) -> str:
+    """Build SAN_LIB (builds the regular objects first if any is missing)."""
+    objs = [os.path.join(OBJDIR, os.path.splitext(s)[0] + ".o") for s in SOURCES]
+    if not all(os.path.exists(o) for o in objs):
+        build(verbose)
+    rocm = os.environ.get("ROCM_PATH", "/opt/rocm")
+    api_obj = os.path.join(OBJDIR, "api_hostsan.o")
+    cc = ["g++", "-std=c++17", "-O1", "-g", "-fPIC", *SAN_FLAGS, "-D__HIP_PLATFORM_AMD__=1",
+          "-I", ROCM_INC, "-I", INCLUDE, "-I", CSRC, "-c", os.path.join(CSRC, "api.cpp"),
+          "-o", api_obj]
+    link = ["g++", "-shared", *SAN_FLAGS, api_obj, *[o for o in objs if not o.endswith("api.o")],
+            "-L", os.path.join(rocm, "lib"), "-lamdhip64", "-Wl,-rpath," + os.path.join(rocm, "lib"),
+            "-o", SAN_LIB]
+    for cmd in (cc, link):
+        r = subprocess.run(cmd, capture_output=True, text=True)
+        if r.returncode != 0:
+            raise RuntimeError(f"sanitized build failed:\n{' '.join(cmd)}\n{r.stdout}{r.stderr}")
+    if verbose:
+        print(f"built {SAN_LIB}")
+    return SAN_LIB
+
+
+def host_sanitizer_env(env=None) -> dict:
+    """Environment that loads SAN_LIB under the ASan runtime.  The runtime is
+    put first in LD_PRELOAD, ahead of whatever the environment already
+    preloads."""
+    env = dict(os.environ if env is None else env)
+    asan = subprocess.run(["g++", "-print-file-name=libasan.so"], capture_output=True,
+                          text=True, check=True).stdout.strip()
+    env["LD_PRELOAD"] = asan + (":" + env["LD_PRELOAD"] if env.get("LD_PRELOAD") else "")
+    env["S2MOE_LIBRARY"] = SAN_LIB
+    env["ASAN_OPTIONS"] = "detect_leaks=0:abort_on_error=1"
+    env["UBSAN_OPTIONS"] = "print_stacktrace=1:halt_on_error=1"
+    return env
+
+
 if __name__ == "__main__":
-    build()
+    if "--host-sanitize" in sys.argv[1:]:
+        build_host_sanitized()
+    else:
+        build()

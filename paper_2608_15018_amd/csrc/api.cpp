@@ -219,10 +219,15 @@ size_t s2moe_workspace_bytes(const s2moe_layer* layer, int32_t n_tokens) {
   return workspace_bytes(layer, n_tokens);
 }
 
-s2moe_status s2moe_verify_moe(const s2moe_layer* layer, int32_t n_tokens, const void* x,
-                              const s2moe_weights* w, const s2moe_routing* r, void* workspace,
-                              size_t workspace_bytes_given, float* expert_out, void* stream) {
-  const char* fn = "s2moe_verify_moe";
+}  // extern "C"
+
+namespace {
+
+// Checks shared by both verify entry points, then everything of the launch
+// except the workspace carve-up.
+s2moe_status verify_args(const char* fn, const s2moe_layer* layer, int32_t n_tokens,
+                         const void* x, const s2moe_weights* w, const s2moe_routing* r,
+                         float* expert_out, s2moe::FfnArgs* out) {
   s2moe_status st = check_layer(fn, layer, n_tokens);
   if (st != S2MOE_OK) return st;
   if (w == nullptr) return fail(S2MOE_EINVAL, "%s: weights is NULL", fn);
@@ -253,16 +258,8 @@ s2moe_status s2moe_verify_moe(const s2moe_layer* layer, int32_t n_tokens, const 
   S2MOE_REQUIRE_PTR(r->slot);
   S2MOE_REQUIRE_PTR(r->uniq);
   S2MOE_REQUIRE_PTR(r->n_uniq);
-  const size_t need = workspace_bytes(layer, n_tokens);
-  if (workspace == nullptr)
-    return fail(S2MOE_EWORKSPACE, "%s: workspace is NULL (%zu bytes needed)", fn, need);
-  if (!aligned16(workspace))
-    return fail(S2MOE_EINVAL, "%s: workspace is not 16-byte aligned", fn);
-  if (workspace_bytes_given < need)
-    return fail(S2MOE_EWORKSPACE, "%s: workspace holds %zu bytes, %zu needed", fn,
-                workspace_bytes_given, need);
 
-  s2moe::FfnArgs a;
+  s2moe::FfnArgs& a = *out;
   a.B = n_tokens;
   a.k = layer->top_k;
   a.S = layer->n_shared;
@@ -290,12 +287,42 @@ s2moe_status s2moe_verify_moe(const s2moe_layer* layer, int32_t n_tokens, const 
   a.sh_gate_s = w->sh_gate_s;
   a.sh_up_s = w->sh_up_s;
   a.sh_down_s = w->sh_down_s;
-  char* ws = static_cast<char*>(workspace);
-  a.hh = ws;
+  a.hh = nullptr;
   a.ldh = (int)hh_ld(layer);
-  a.x16 = q4 ? ws + hh_bytes(layer, n_tokens) : nullptr;
+  a.x16 = nullptr;
   a.out = expert_out;
   a.packed = (layer->flags & S2MOE_PACKED_WEIGHTS) != 0;
+  return S2MOE_OK;
+}
+
+// Hh at the start of the workspace, then (int4 weights) the fp16 copy of x.
+void carve_workspace(const s2moe_layer* layer, int32_t n_tokens, void* workspace,
+                     s2moe::FfnArgs* a) {
+  char* ws = static_cast<char*>(workspace);
+  a->hh = ws;
+  a->x16 = layer->w_dtype == S2MOE_Q4G32 ? ws + hh_bytes(layer, n_tokens) : nullptr;
+}
+
+}  // namespace
+
+extern "C" {
+
+s2moe_status s2moe_verify_moe(const s2moe_layer* layer, int32_t n_tokens, const void* x,
+                              const s2moe_weights* w, const s2moe_routing* r, void* workspace,
+                              size_t workspace_bytes_given, float* expert_out, void* stream) {
+  const char* fn = "s2moe_verify_moe";
+  s2moe::FfnArgs a;
+  s2moe_status st = verify_args(fn, layer, n_tokens, x, w, r, expert_out, &a);
+  if (st != S2MOE_OK) return st;
+  const size_t need = workspace_bytes(layer, n_tokens);
+  if (workspace == nullptr)
+    return fail(S2MOE_EWORKSPACE, "%s: workspace is NULL (%zu bytes needed)", fn, need);
+  if (!aligned16(workspace))
+    return fail(S2MOE_EINVAL, "%s: workspace is not 16-byte aligned", fn);
+  if (workspace_bytes_given < need)
+    return fail(S2MOE_EWORKSPACE, "%s: workspace holds %zu bytes, %zu needed", fn,
+                workspace_bytes_given, need);
+  carve_workspace(layer, n_tokens, workspace, &a);
   return hip_status(fn, s2moe::launch_ffn(a, static_cast<hipStream_t>(stream)));
 }
 
@@ -472,6 +499,15 @@ s2moe_status s2moe_combine(const s2moe_layer* layer, int32_t n_tokens, const s2m
   S2MOE_REQUIRE_PTR(r->gate_w);
   S2MOE_REQUIRE_PTR(expert_out);
   S2MOE_REQUIRE_PTR(y);
+  {
+    const size_t H = (size_t)layer->hidden, B = (size_t)n_tokens;
+    const char* e0 = reinterpret_cast<const char*>(expert_out);
+    const char* y0 = reinterpret_cast<const char*>(y);
+    const size_t eb = (B * layer->top_k + (size_t)layer->n_shared * B) * H * sizeof(float);
+    const size_t yb = B * H * sizeof(float);
+    if (y0 < e0 + eb && e0 < y0 + yb)
+      return fail(S2MOE_EINVAL, "%s: y overlaps expert_out", fn);
+  }
   s2moe::CombineArgs a;
   a.gate_w = r->gate_w;
   a.expert_out = expert_out;

@@ -242,8 +242,10 @@ __global__ __launch_bounds__(1024) void reuse_gate_kernel(GateArgs a) {
 
   // Stable expert-major slot list: assignment (b, j) of expert e goes after
   // the assignments of e by tokens b' < b.  Every idx_s entry was written
-  // above with an id below E; the clamps keep the addressing inside offset_s
-  // and slot even if that ever stopped holding.
+  // above with an id below E, and offset_s[e] + before < B k for each of
+  // them, so the two clamps below never change a result the kernel computes.
+  // They are defence only: they keep the addressing inside offset_s and slot
+  // should that invariant ever be broken by a change to this kernel.
   for (int i = tid; i < B * k; i += blockDim.x) {
     const int b = i / k;
     const int e = min((int)idx_s[i], E - 1);

@@ -210,3 +210,16 @@ def test_expand_row_index_shortcut_exhaustive():
         magic = np.uint64(((1 << 42) + k - 1) // k)
         assert ((f * magic) >> np.uint64(42) == f // np.uint64(k)).all(), k
         assert int(magic) * ((1 << 22) - 1) < 2 ** 64
+
+
+def test_combine_rejects_overlapping_output(lib):
+    L = _layer(n_shared=1, ffn_shared=512)
+    B, H = 4, 256
+    rt = _lib.RoutingStruct(*([0x200000] * 12))
+    eo = 0x1000000
+    eo_bytes = (B * 2 + B) * H * 4
+    for y in (eo, eo + eo_bytes - 16, eo - B * H * 4 + 16):
+        st = lib.s2moe_combine(ctypes.byref(L), B, ctypes.byref(rt), ctypes.c_void_p(eo),
+                               ctypes.c_void_p(y), None)
+        assert st == _lib.EINVAL and "overlaps" in _lib.last_error()
+

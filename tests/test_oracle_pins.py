@@ -8,6 +8,7 @@ oracle fails at least one of them.
 """
 
 import itertools
+import math
 
 import numpy as np
 import pytest
@@ -84,22 +85,61 @@ def test_ties_break_toward_lower_expert_index():
 
 
 # ---------------------------------------------------------------- gating (a3-a5)
-def brute_gate(ell, w, k, cap, alpha):
-    """Independent gating by subset enumeration."""
+ACT_ONLY, ABSOLUTE, FROM_BIASED = 1, 2, 4      # the flag values of the C ABI
+
+
+def brute_gate(ell, w, k, cap, alpha, flags=0):
+    """Independent gating by subset enumeration, in plain Python floats.
+
+    Sec. "Reuse-aware Expert Gating": confidences enter g only as
+    non-negative weights, so w_b < 0 counts as 0 and, when no w_b is
+    positive, no expert is preferred and no bias applies.  E* is the cap-subset
+    of the candidates with the largest total g (the candidates are all experts,
+    or with ACT_ONLY the union of the plain top-k sets; every candidate when
+    there are at most cap of them).  The bias is alpha * (top-1 minus (k+1)-th
+    logit), or alpha itself with ABSOLUTE.  The gate weights are exp(z_j) /
+    sum_j exp(z_j) over the selected experts, z the original logits or, with
+    FROM_BIASED, the biased ones."""
     B, E = ell.shape
-    g = [sum(max(w[b], 0.0) * ell[b][e] for b in range(B)) for e in range(E)]
-    pref = set(brute_topk(g, cap))
-    idx = []
+    wc = [float(w[b]) if w[b] > 0 else 0.0 for b in range(B)]
+    active = any(v > 0.0 for v in wc)
+    g = [sum(wc[b] * float(ell[b][e]) for b in range(B)) for e in range(E)]
+    plain = [brute_topk([float(v) for v in ell[b]], k) for b in range(B)]
+    if not active:
+        pref = set()
+    else:
+        cand = sorted(set().union(*map(set, plain))) if flags & ACT_ONLY else list(range(E))
+        if len(cand) <= cap:
+            pref = set(cand)
+        else:
+            pref = set(max(itertools.combinations(cand, cap),
+                           key=lambda s: sum(g[e] for e in s)))
+    idx, gw = [], []
     for b in range(B):
-        desc = sorted(ell[b], reverse=True)
-        lam = alpha * (desc[0] - desc[k])
-        val = [ell[b][e] + (lam if e in pref else 0.0) for e in range(E)]
-        idx.append(brute_topk(val, k))
-    return pref, idx
+        row = [float(v) for v in ell[b]]
+        desc = sorted(row, reverse=True)
+        if not active:
+            lam = 0.0
+        elif flags & ABSOLUTE:
+            lam = alpha
+        else:
+            lam = alpha * (desc[0] - desc[k])
+        val = [row[e] + (lam if e in pref else 0.0) for e in range(E)]
+        sel = brute_topk(val, k)
+        src = val if flags & FROM_BIASED else row
+        ez = [math.exp(src[e]) for e in sel]
+        idx.append(sel)
+        gw.append([v / sum(ez) for v in ez])
+    return {"g": g, "pref": pref, "idx": idx, "gate_w": gw}
 
 
-@pytest.mark.parametrize("seed", range(30))
-def test_reuse_gate_bruteforce(seed):
+GATE_FLAGS = (0, ACT_ONLY, ABSOLUTE, FROM_BIASED, ACT_ONLY | ABSOLUTE | FROM_BIASED)
+W_MODES = ("nonneg", "mixed", "nonpos")
+
+
+def gate_case(seed, w_mode):
+    """A small gating problem: logits with distinct subset sums, confidences
+    drawn >= 0, of mixed sign (mostly one positive or more), or all <= 0."""
     rng = np.random.default_rng(100 + seed)
     E = int(rng.integers(4, 9))
     k = int(rng.integers(1, min(3, E - 1) + 1))
@@ -107,19 +147,44 @@ def test_reuse_gate_bruteforce(seed):
     B = int(rng.integers(1, 7))
     alpha = float(rng.choice([0.0, 0.3, 0.5, 0.9, 2.0]))
     ell = _distinct(rng, (B, E))
-    w = rng.random(B)
-    gap = np.array([sorted(row, reverse=True)[0] - sorted(row, reverse=True)[k] for row in ell])
-    plain = np.array([sorted(brute_topk(list(row), k)) for row in ell])
-    gt = oracle.reuse_gate(ell, gap, plain, w, k, cap, alpha)
-    pref, idx = brute_gate(ell, w, k, cap, alpha)
-    assert set(np.nonzero(gt["pref"])[0]) == pref
-    assert [list(r) for r in gt["idx"]] == idx
-    # g pinned by one-hot confidences: g = ell_b0
-    b0 = int(rng.integers(0, B))
-    onehot = np.zeros(B)
+    if w_mode == "nonneg":
+        w = rng.random(B)
+    elif w_mode == "mixed":
+        w = rng.standard_normal(B)
+        w[int(rng.integers(0, B))] = rng.random() + 0.1    # at least one positive
+    else:
+        w = -rng.random(B) * (rng.random(B) < 0.7)          # negatives and zeros
+    return ell, w, k, cap, alpha
+
+
+def check_gate_case(O_mod, seed, flags, w_mode):
+    """Compare O_mod.reuse_gate with brute_gate on one case; raise
+    AssertionError on any difference."""
+    ell, w, k, cap, alpha = gate_case(seed, w_mode)
+    desc = [sorted(row, reverse=True) for row in ell]
+    gap = np.array([d[0] - d[k] for d in desc])
+    plain = np.array([brute_topk(list(row), k) for row in ell])
+    gt = O_mod.reuse_gate(ell, gap, plain, w, k, cap, alpha, flags)
+    ref = brute_gate(ell, w, k, cap, alpha, flags)
+    np.testing.assert_allclose(gt["g"], ref["g"], rtol=1e-12, atol=1e-12)
+    assert set(np.nonzero(gt["pref"])[0]) == ref["pref"]
+    assert [list(r) for r in gt["idx"]] == ref["idx"]
+    np.testing.assert_allclose(gt["gate_w"], ref["gate_w"], rtol=1e-12, atol=0)
+    # g pinned by one-hot confidences: g = 0.7 ell_b0, whatever the others'
+    # (non-positive) values
+    rng = np.random.default_rng(seed)
+    b0 = int(rng.integers(0, ell.shape[0]))
+    onehot = np.minimum(w, 0.0)
     onehot[b0] = 0.7
-    g1 = oracle.reuse_gate(ell, gap, plain, onehot, k, cap, alpha)["g"]
+    g1 = O_mod.reuse_gate(ell, gap, plain, onehot, k, cap, alpha, flags)["g"]
     np.testing.assert_allclose(g1, 0.7 * ell[b0], rtol=0, atol=1e-15)
+
+
+@pytest.mark.parametrize("w_mode", W_MODES)
+@pytest.mark.parametrize("flags", GATE_FLAGS)
+@pytest.mark.parametrize("seed", range(30))
+def test_reuse_gate_bruteforce(seed, flags, w_mode):
+    check_gate_case(O, seed, flags, w_mode)
 
 
 def test_bias_is_alpha_times_top1_minus_kplus1_gap():
