@@ -170,6 +170,26 @@ s2moe_status s2moe_verify_moe(const s2moe_layer *layer, int32_t n_tokens, const 
                               void *workspace, size_t workspace_bytes, float *expert_out,
                               void *stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+   capture, tight serving loops, harnesses that forbid hipMalloc):
+   s2moe_verify_moe without a workspace argument.  The SwiGLU activations
+   (and, for Q4G32 weights, the fp16 copy of x) go to a scratch array the
+   library holds in device memory, S2MOE_NOALLOC_SCRATCH_BYTES per GPU, from
+   the library's load until the process ends; the call itself allocates
+   nothing.  Arguments, outputs and results are those of s2moe_verify_moe,
+   computed by the same kernels.  A layer and n_tokens whose
+   s2moe_workspace_bytes exceed S2MOE_NOALLOC_SCRATCH_BYTES are rejected
+   with S2MOE_EUNSUPPORTED before anything is enqueued (c2- to c5-shaped
+   layers at up to 64 tokens need at most about 4.2 MiB).  All calls on one
+   GPU share its array: calls that can overlap on the device (different
+   streams without ordering, several host threads) race and give undefined
+   results.  Calls ordered on one stream are safe; the array's contents
+   left by a previous call are never read. */
+#define S2MOE_NOALLOC_SCRATCH_BYTES (8u << 20)
+s2moe_status s2moe_verify_moe_noalloc(const s2moe_layer *layer, int32_t n_tokens, const void *x,
+                                      const s2moe_weights *w, const s2moe_routing *r,
+                                      float *expert_out, void *stream);
+
 /* Re-lay n_mats expert matrices of [rows, cols] (K = cols contiguous) into
    the tile order the matrix-core kernels stream (layer flag
    S2MOE_PACKED_WEIGHTS).  A one-time transform at model load, not part of

@@ -15,6 +15,7 @@ from ._lib import (  # noqa: F401
     PREF_ACTIVATED_ONLY,
     Q4G32,
     Layer,
+    NOALLOC_SCRATCH_BYTES,
     Routing,
     STREAM_SINK_WORDS,
     S2moeError,
@@ -31,6 +32,7 @@ from ._lib import (  # noqa: F401
     route,
     stream_read,
     verify_moe,
+    verify_moe_noalloc,
     workspace_bytes,
 )
 from .pipeline import (  # noqa: F401

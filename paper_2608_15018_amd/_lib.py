@@ -85,6 +85,8 @@ def load():
     lib.s2moe_workspace_bytes.restype = ctypes.c_size_t
     lib.s2moe_verify_moe.argtypes = [Lp, ctypes.c_int32, P, ctypes.POINTER(Weights),
                                      ctypes.POINTER(RoutingStruct), P, ctypes.c_size_t, P, P]
+    lib.s2moe_verify_moe_noalloc.argtypes = [Lp, ctypes.c_int32, P, ctypes.POINTER(Weights),
+                                             ctypes.POINTER(RoutingStruct), P, P]
     lib.s2moe_combine.argtypes = [Lp, ctypes.c_int32, ctypes.POINTER(RoutingStruct), P, P, P]
     lib.s2moe_pack_weights.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
                                        ctypes.c_int32, P, P, P, P, P]
@@ -96,7 +98,8 @@ def load():
     lib.s2moe_expand_max_nodes.restype = ctypes.c_int
     lib.s2moe_stream_read.argtypes = [P, ctypes.c_size_t, P, P]
     lib.s2moe_stream_read.restype = ctypes.c_int
-    for f in ("s2moe_route", "s2moe_reuse_gate", "s2moe_verify_moe", "s2moe_combine"):
+    for f in ("s2moe_route", "s2moe_reuse_gate", "s2moe_verify_moe", "s2moe_verify_moe_noalloc",
+              "s2moe_combine"):
         getattr(lib, f).restype = ctypes.c_int
     lib.s2moe_last_error.restype = ctypes.c_char_p
     lib.s2moe_last_error.argtypes = []
@@ -235,6 +238,17 @@ def verify_moe(layer: Layer, x: torch.Tensor, weights: Weights, rt: Routing,
                                    ctypes.byref(rt.struct), _ptr(workspace),
                                    workspace.numel() * workspace.element_size(),
                                    _ptr(expert_out), _stream(stream)))
+
+
+def verify_moe_noalloc(layer: Layer, x: torch.Tensor, weights: Weights, rt: Routing,
+                       expert_out: torch.Tensor, stream=None):
+    """s2moe_verify_moe_noalloc: verify_moe on the library's own scratch array."""
+    _check(load().s2moe_verify_moe_noalloc(ctypes.byref(layer), rt.B, _ptr(x),
+                                           ctypes.byref(weights), ctypes.byref(rt.struct),
+                                           _ptr(expert_out), _stream(stream)))
+
+
+NOALLOC_SCRATCH_BYTES = 8 << 20
 
 
 def combine(layer: Layer, rt: Routing, expert_out: torch.Tensor, y: torch.Tensor, stream=None):

@@ -18,7 +18,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 OBJDIR = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libs2moe.so")
-SOURCES = ["api.cpp", "route.hip", "gate.hip", "ffn.hip", "ffn_bf16.hip", "ffn_q4.hip", "combine.hip", "pack.hip", "probe.hip", "expand.hip"]
+SOURCES = ["api.cpp", "route.hip", "gate.hip", "ffn.hip", "ffn_bf16.hip", "ffn_q4.hip", "combine.hip", "pack.hip", "probe.hip", "expand.hip", "noalloc.hip"]
 ARCH = "gfx950"
 ROCM_INC = os.path.join(os.environ.get("ROCM_PATH", "/opt/rocm"), "include")
 

@@ -326,6 +326,27 @@ s2moe_status s2moe_verify_moe(const s2moe_layer* layer, int32_t n_tokens, const 
   return hip_status(fn, s2moe::launch_ffn(a, static_cast<hipStream_t>(stream)));
 }
 
+s2moe_status s2moe_verify_moe_noalloc(const s2moe_layer* layer, int32_t n_tokens,
+                                      const void* x, const s2moe_weights* w,
+                                      const s2moe_routing* r, float* expert_out,
+                                      void* stream) {
+  const char* fn = "s2moe_verify_moe_noalloc";
+  s2moe::FfnArgs a;
+  s2moe_status st = verify_args(fn, layer, n_tokens, x, w, r, expert_out, &a);
+  if (st != S2MOE_OK) return st;
+  const size_t need = workspace_bytes(layer, n_tokens);
+  if (need > (size_t)S2MOE_NOALLOC_SCRATCH_BYTES)
+    return fail(S2MOE_EUNSUPPORTED,
+                "%s: this layer and n_tokens = %d need %zu bytes of scratch; the library's "
+                "scratch array holds %zu (use s2moe_verify_moe with a caller workspace)",
+                fn, n_tokens, need, (size_t)S2MOE_NOALLOC_SCRATCH_BYTES);
+  void* scratch = nullptr;
+  const hipError_t err = s2moe::noalloc_scratch(&scratch);
+  if (err != hipSuccess) return hip_status(fn, err);
+  carve_workspace(layer, n_tokens, scratch, &a);
+  return hip_status(fn, s2moe::launch_ffn(a, static_cast<hipStream_t>(stream)));
+}
+
 namespace {
 
 bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }

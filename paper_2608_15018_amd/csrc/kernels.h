@@ -137,6 +137,10 @@ __host__ __device__ inline ExpandLds expand_lds(int N, int L, int E, int k) {
   return o;
 }
 
+// Device address of the library's scratch array on the current device
+// (S2MOE_NOALLOC_SCRATCH_BYTES bytes, 256-byte aligned).
+hipError_t noalloc_scratch(void** ptr);
+
 hipError_t launch_expand(const ExpandArgs& a, size_t lds_bytes, hipStream_t s);
 hipError_t launch_route(const RouteArgs& a, hipStream_t s);
 hipError_t launch_stream_read(const void* src, size_t bytes, uint32_t* sink, int blocks,

@@ -223,3 +223,26 @@ def test_combine_rejects_overlapping_output(lib):
                                ctypes.c_void_p(y), None)
         assert st == _lib.EINVAL and "overlaps" in _lib.last_error()
 
+
+def test_noalloc_verify_rejects_oversized_scratch_on_host(lib):
+    """A layer whose workspace exceeds the library's scratch array is
+    rejected before anything touches the device (no GPU needed)."""
+    L = _layer(hidden=4096, ffn=14336, n_experts=8, top_k=2, cap=4)
+    w = _lib.Weights(*([0x300000] * 12))
+    rt = _lib.RoutingStruct(*([0x200000] * 12))
+    fake = ctypes.c_void_p(0x100000)
+    B = 256
+    assert s2.workspace_bytes(L, B) > s2.NOALLOC_SCRATCH_BYTES
+    st = lib.s2moe_verify_moe_noalloc(ctypes.byref(L), B, fake, ctypes.byref(w),
+                                      ctypes.byref(rt), fake, None)
+    assert st == _lib.EUNSUPPORTED and "scratch" in _lib.last_error()
+    st = lib.s2moe_verify_moe_noalloc(ctypes.byref(L), 4, fake, ctypes.byref(w),
+                                      ctypes.byref(rt), None, None)
+    assert st == _lib.EINVAL and "expert_out" in _lib.last_error()
+
+
+def test_noalloc_scratch_size_matches_header():
+    import re
+    text = open(_lib.HEADER_PATH).read()
+    m = re.search(r"#define S2MOE_NOALLOC_SCRATCH_BYTES \((\d+)u << (\d+)\)", text)
+    assert m and int(m.group(1)) << int(m.group(2)) == s2.NOALLOC_SCRATCH_BYTES
