@@ -99,7 +99,8 @@ s2moe_status check_layer(const char* fn, const s2moe_layer* L, int32_t B) {
 size_t round256(size_t n) { return (n + 255) & ~(size_t)255; }
 
 // Workspace: the SwiGLU activations Hh [B*k + S*B, max(F, F_s)] (fp32 for
-// fp32 weights, else 16-bit); for int4 weights then an fp16 copy of x.
+// fp32 weights, else 16-bit); for int4 weights then an fp16 copy of x and
+// the down projection's partial sums.
 size_t hh_rows(const s2moe_layer* L, int32_t B) {
   return (size_t)B * L->top_k + (size_t)L->n_shared * B;
 }
@@ -117,9 +118,20 @@ size_t x16_bytes(const s2moe_layer* L, int32_t B) {
   return round256((size_t)B * L->hidden * 2);
 }
 
+int q4_parts(const s2moe_layer* L, int32_t B) {
+  return s2moe::q4_down_parts(B, L->top_k, L->n_experts, L->hidden, L->ffn, L->n_shared,
+                              L->n_shared > 0 ? L->ffn_shared : 0);
+}
+
+// int4 weights: partial sums of the down projection's K parts 1 .. Q-1.
+size_t part_bytes(const s2moe_layer* L, int32_t B) {
+  if (L->w_dtype != S2MOE_Q4G32) return 0;
+  return round256((size_t)(q4_parts(L, B) - 1) * hh_rows(L, B) * L->hidden * sizeof(float));
+}
+
 size_t workspace_bytes(const s2moe_layer* L, int32_t B) {
   size_t n = hh_bytes(L, B);
-  if (L->w_dtype == S2MOE_Q4G32) n += x16_bytes(L, B);
+  if (L->w_dtype == S2MOE_Q4G32) n += x16_bytes(L, B) + part_bytes(L, B);
   return n;
 }
 
@@ -290,17 +302,24 @@ s2moe_status verify_args(const char* fn, const s2moe_layer* layer, int32_t n_tok
   a.hh = nullptr;
   a.ldh = (int)hh_ld(layer);
   a.x16 = nullptr;
+  a.part = nullptr;
+  a.qparts = q4 ? q4_parts(layer, n_tokens) : 1;
   a.out = expert_out;
   a.packed = (layer->flags & S2MOE_PACKED_WEIGHTS) != 0;
   return S2MOE_OK;
 }
 
-// Hh at the start of the workspace, then (int4 weights) the fp16 copy of x.
+// Hh at the start of the workspace, then (int4 weights) the fp16 copy of x
+// and the down partial sums.
 void carve_workspace(const s2moe_layer* layer, int32_t n_tokens, void* workspace,
                      s2moe::FfnArgs* a) {
   char* ws = static_cast<char*>(workspace);
   a->hh = ws;
-  a->x16 = layer->w_dtype == S2MOE_Q4G32 ? ws + hh_bytes(layer, n_tokens) : nullptr;
+  const bool q4 = layer->w_dtype == S2MOE_Q4G32;
+  a->x16 = q4 ? ws + hh_bytes(layer, n_tokens) : nullptr;
+  a->part = q4 ? reinterpret_cast<float*>(ws + hh_bytes(layer, n_tokens) +
+                                          x16_bytes(layer, n_tokens))
+               : nullptr;
 }
 
 }  // namespace

@@ -11,16 +11,37 @@
 // 1032, or a fused (h / 16) - 72), and a packed multiply by the group scale
 // gives round_fp16(s * (q - 8)).  The four dwords are the A operands of four
 // v_mfma_f32_16x16x32_f16, accumulated in fp32, so no dequantised weight is
-// ever written to memory and no per-group epilogue is needed.  The decode
-// yields the slot order (0,4,1,5,2,6,3,7) inside each 8-element block; the
-// activations are kept in fp16 in that same order (a prep kernel converts x,
-// the gate-up epilogue writes Hh so), with the 8-blocks of each super-step
-// stored so that every B-operand load reads 64 contiguous bytes per token.
+// ever written to memory.  The decode yields the slot order (0,4,1,5,2,6,3,7)
+// inside each 8-element block; the activations are kept in fp16 in that same
+// order (a prep kernel converts x, the gate-up epilogue writes Hh so), with
+// the 8-blocks of each super-step stored so that one token's 16 bytes for
+// MFMA j of the four K slots lie side by side.
 //
-// Work decomposition as in the bf16 kernel: R 16-row tiles per unit, W waves
-// split K, two-stage register pipeline, LDS reduction in wave order.  Above
-// 8 tokens the gate-up launch instead uses a row-split kernel whose waves
-// share LDS-staged activations (ffn_q4_rows_kernel).
+// Work decomposition (one persistent launch per projection):
+// - A work item is 16 R W rows of one expert (W = 4 waves, R row tiles per
+//   wave) over one of Q contiguous K parts, for all tokens routed to that
+//   expert.  The launch has at most as many workgroups as fit on the GPU at
+//   once; each takes items blockIdx.x, + gridDim.x, ... until the activated
+//   experts' items run out.  (Measured on MI355X: dealing equal runs of
+//   consecutive items, or one workgroup per item, was 3-15 % slower.)
+// - The waves of a workgroup stream different rows over the same K range, so
+//   they share the activations: the workgroup stages the tokens' next
+//   super-step in LDS while the current one is decoded (double-buffered, one
+//   barrier per super-step), and every B operand is an LDS read.  Reading
+//   them with one global load per MFMA instead caps the stream at a fraction
+//   of HBM bandwidth on MI355X (measured: 3.8 TB/s at one token tile, 1 TB/s
+//   at four).
+// - Each wave keeps D - 1 super-steps of codes in flight in a register ring
+//   (D = 2: the decode, not the memory latency, bounds the stream; deeper
+//   rings of 3, 4, 6 and 8 were 2-35 % slower on MI355X as their registers
+//   cost occupancy).
+// - Up to TMAX = 4 token tiles (64 tokens) share one pass over the weights;
+//   larger buckets take further passes.
+// - Gate-up items span all of K (Q = 1), so SwiGLU is applied in the
+//   epilogue.  Down items split K into Q parts when few experts are active:
+//   part 0 writes expert_out, parts 1..Q-1 write partial sums to the
+//   workspace, and q4_reduce_kernel adds them in part order afterwards, so
+//   the result does not depend on timing.
 #include <atomic>
 
 #include "ffn_common.h"
@@ -33,6 +54,8 @@ namespace {
 
 typedef _Float16 half2v __attribute__((ext_vector_type(2)));
 typedef _Float16 half8v __attribute__((ext_vector_type(8)));
+
+constexpr int kW = 4;  // waves per workgroup
 
 __device__ __forceinline__ f32x4 mfma16(half8v a, half8v b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
@@ -86,221 +109,16 @@ __device__ __forceinline__ half8v q4_decode(uint32_t w, half2v s2, uint32_t magi
   return r;
 }
 
-template <int T, int R, int NM>
-struct StageQ {
+// Codes and scales of one super-step for the wave's NM x R row tiles.
+template <int R, int NM>
+struct CodesQ {
   u32x4 c[NM][R];     // one 32-code group per lane
   uint32_t s[NM][R];  // its fp16 scale (low half)
-  u32x4 b[T][4];      // 4 x 8 activations per token tile
 };
 
 // Codes and scale of super-step s: plain layout -> u32x4 index 4 s and
 // scale index 4 s of the lane's row pointers; packed layout -> 1 KB code
 // tile s and 128-byte scale tile s (nontemporal: read once per call).
-template <bool kPacked, int T, int R, int NM>
-__device__ __forceinline__ void load_q(StageQ<T, R, NM>& st, const u32x4* const* pc,
-                                       const uint16_t* const* ps, const u32x4* const* xb,
-                                       int s) {
-#pragma unroll
-  for (int m = 0; m < NM; ++m)
-#pragma unroll
-    for (int r = 0; r < R; ++r) {
-      if (kPacked) {
-        st.c[m][r] = __builtin_nontemporal_load(pc[m * R + r] + 64 * s);
-        st.s[m][r] = __builtin_nontemporal_load(ps[m * R + r] + 64 * s);
-      } else {
-        st.c[m][r] = pc[m * R + r][4 * s];
-        st.s[m][r] = ps[m * R + r][4 * s];
-      }
-    }
-#pragma unroll
-  for (int tt = 0; tt < T; ++tt)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) st.b[tt][j] = xb[tt][16 * s + 4 * j];
-}
-
-template <int T, int R, int NM>
-__device__ __forceinline__ void compute_q(const StageQ<T, R, NM>& st, f32x4 (&acc)[NM][R][T],
-                                          uint32_t magic) {
-#pragma unroll
-  for (int m = 0; m < NM; ++m)
-#pragma unroll
-    for (int r = 0; r < R; ++r) {
-      _Float16 sh;
-      const uint16_t bits = (uint16_t)st.s[m][r];
-      __builtin_memcpy(&sh, &bits, 2);
-      const half2v s2 = {sh, sh};
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const half8v a = q4_decode(st.c[m][r][j], s2, magic);
-#pragma unroll
-        for (int tt = 0; tt < T; ++tt)
-          acc[m][r][tt] = mfma16(a, as_half8(st.b[tt][j]), acc[m][r][tt]);
-      }
-    }
-}
-
-template <int kMode, int T, int TMAX, int R, int W, bool kPacked>
-__device__ __forceinline__ void unit_pass_q(const FfnArgs& a, const Segment& seg, int t0, int r0,
-                                            int K, const uint8_t* C0, const uint8_t* C1,
-                                            const uint16_t* S0, const uint16_t* S1, f32x4* red) {
-  constexpr int NM = kMode == 0 ? 2 : 1;
-  const int lane = threadIdx.x & (kWave - 1);
-  const int wave = wave_id();
-  const int rA = lane & 15, gK = lane >> 4;
-  const int nss = K / 128;
-  const int lo = wave * nss / W, hi = (wave + 1) * nss / W;
-
-  // fp16 activations in decode order: x16 for gate-up, Hh for down.
-  const uint16_t* X = static_cast<const uint16_t*>(kMode == 0 ? a.x16 : a.hh);
-  const int ldx = kMode == 0 ? a.H : a.ldh;
-  const u32x4* xb[T];
-#pragma unroll
-  for (int tt = 0; tt < T; ++tt) {
-    const int t = min(t0 + tt * 16 + rA, seg.n - 1);
-    xb[tt] = reinterpret_cast<const u32x4*>(X + (size_t)x_row(a, kMode, seg, t) * ldx) + gK;
-  }
-  const u32x4* pc[NM * R];
-  const uint16_t* ps[NM * R];
-#pragma unroll
-  for (int r = 0; r < R; ++r) {
-    if (kPacked) {
-      const size_t tile0 = (size_t)(r0 / 16 + r) * nss;  // first tile of the row tile
-      pc[r] = reinterpret_cast<const u32x4*>(C0) + tile0 * 64 + lane;
-      ps[r] = S0 + tile0 * 64 + lane;
-      if (NM > 1) {
-        pc[R + r] = reinterpret_cast<const u32x4*>(C1) + tile0 * 64 + lane;
-        ps[R + r] = S1 + tile0 * 64 + lane;
-      }
-    } else {
-      const size_t row = (size_t)(r0 + 16 * r + rA);
-      pc[r] = reinterpret_cast<const u32x4*>(C0 + row * (K / 2)) + gK;
-      ps[r] = S0 + row * (K / 32) + gK;
-      if (NM > 1) {
-        pc[R + r] = reinterpret_cast<const u32x4*>(C1 + row * (K / 2)) + gK;
-        ps[R + r] = S1 + row * (K / 32) + gK;
-      }
-    }
-  }
-
-  f32x4 acc[NM][R][T];
-#pragma unroll
-  for (int m = 0; m < NM; ++m)
-#pragma unroll
-    for (int r = 0; r < R; ++r)
-#pragma unroll
-      for (int tt = 0; tt < T; ++tt) acc[m][r][tt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  if (hi > lo) {
-    const uint32_t magic = opaque(0x64006400u);
-    pipeline2<StageQ<T, R, NM>>(
-        hi - lo,
-        [&](StageQ<T, R, NM>& st, int i) { load_q<kPacked>(st, pc, ps, xb, lo + i); },
-        [&](const StageQ<T, R, NM>& st, int) { compute_q(st, acc, magic); });
-  }
-
-  if (W > 1) {
-    constexpr int kTiles = NM * R * TMAX;
-#pragma unroll
-    for (int m = 0; m < NM; ++m)
-#pragma unroll
-      for (int r = 0; r < R; ++r)
-#pragma unroll
-        for (int tt = 0; tt < T; ++tt)
-          red[(wave * kTiles + (m * R + r) * TMAX + tt) * kWave + lane] = acc[m][r][tt];
-    __syncthreads();
-    if (wave == 0) {
-      for (int w = 1; w < W; ++w) {
-#pragma unroll
-        for (int m = 0; m < NM; ++m)
-#pragma unroll
-          for (int r = 0; r < R; ++r)
-#pragma unroll
-            for (int tt = 0; tt < T; ++tt) {
-              const f32x4 p = red[(w * kTiles + (m * R + r) * TMAX + tt) * kWave + lane];
-#pragma unroll
-              for (int i = 0; i < 4; ++i) acc[m][r][tt][i] += p[i];
-            }
-      }
-    }
-  }
-  if (wave == 0) {
-#pragma unroll
-    for (int tt = 0; tt < T; ++tt) {
-      const int t = t0 + tt * 16 + rA;
-      if (t >= seg.n) continue;
-      if (kMode == 0) {
-        _Float16* dst = static_cast<_Float16*>(a.hh) + (size_t)(seg.base + t) * a.ldh;
-#pragma unroll
-        for (int r = 0; r < R; ++r)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int f = r0 + 16 * r + 4 * gK + i;
-            dst[(block_pos(f >> 3) << 3) | pos8(f & 7)] =
-                (_Float16)(silu(acc[0][r][tt][i]) * acc[NM - 1][r][tt][i]);
-          }
-      } else {
-        float* dst = a.out + (size_t)out_row(a, seg, t) * a.H;
-#pragma unroll
-        for (int r = 0; r < R; ++r)
-          *reinterpret_cast<f32x4*>(dst + r0 + 16 * r + 4 * gK) = acc[0][r][tt];
-      }
-    }
-  }
-  if (W > 1) __syncthreads();
-}
-
-template <int kMode, int TMAX, int R, int W, bool kPacked>
-__global__ __launch_bounds__(W * 64) void ffn_q4_kernel(FfnArgs a) {
-  constexpr int NM = kMode == 0 ? 2 : 1;
-  __shared__ f32x4 red[W > 1 ? W * NM * R * TMAX * kWave : 1];
-  Segment seg;
-  int unit;
-  if (!resolve_block(a, kMode, 16 * R, &seg, &unit)) return;
-  const int r0 = unit * 16 * R;
-  const int rows = kMode == 0 ? (seg.shared ? a.Fs : a.F) : a.H;
-  const int K = kMode == 0 ? a.H : (seg.shared ? a.Fs : a.F);
-  const size_t mat = (size_t)rows * K;
-  const void *M0, *M1, *Q0, *Q1;
-  if (kMode == 0) {
-    M0 = seg.shared ? a.sh_gate : a.gate;
-    M1 = seg.shared ? a.sh_up : a.up;
-    Q0 = seg.shared ? a.sh_gate_s : a.gate_s;
-    Q1 = seg.shared ? a.sh_up_s : a.up_s;
-  } else {
-    M0 = M1 = seg.shared ? a.sh_down : a.down;
-    Q0 = Q1 = seg.shared ? a.sh_down_s : a.down_s;
-  }
-  const uint8_t* C0 = static_cast<const uint8_t*>(M0) + seg.id * (mat / 2);
-  const uint8_t* C1 = static_cast<const uint8_t*>(M1) + seg.id * (mat / 2);
-  const uint16_t* S0 = static_cast<const uint16_t*>(Q0) + seg.id * (mat / 32);
-  const uint16_t* S1 = static_cast<const uint16_t*>(Q1) + seg.id * (mat / 32);
-  for (int t0 = 0; t0 < seg.n; t0 += 16 * TMAX) {
-    const int T = min(TMAX, (seg.n - t0 + 15) / 16);
-    if (TMAX >= 4 && T >= 4)
-      unit_pass_q<kMode, (TMAX >= 4 ? 4 : 1), TMAX, R, W, kPacked>(a, seg, t0, r0, K, C0, C1, S0, S1, red);
-    else if (TMAX >= 3 && T == 3)
-      unit_pass_q<kMode, (TMAX >= 3 ? 3 : 1), TMAX, R, W, kPacked>(a, seg, t0, r0, K, C0, C1, S0, S1, red);
-    else if (TMAX >= 2 && T == 2)
-      unit_pass_q<kMode, (TMAX >= 2 ? 2 : 1), TMAX, R, W, kPacked>(a, seg, t0, r0, K, C0, C1, S0, S1, red);
-    else
-      unit_pass_q<kMode, 1, TMAX, R, W, kPacked>(a, seg, t0, r0, K, C0, C1, S0, S1, red);
-  }
-}
-
-// Row-split variant (one or two token tiles per pass): the W waves of a
-// workgroup take different row tiles over all of K, and share the
-// activations, which the workgroup stages in LDS two super-steps at a time
-// (double-buffered, one barrier per two super-steps).  The B operands then
-// come from LDS instead of one global load per wave, which at two token
-// tiles would move twice the weight bytes through the texture units.
-constexpr int kChunkU4 = 32;       // u32x4 of one token row per chunk (2 super-steps)
-constexpr int kLdsRowU4 = kChunkU4 + 1;  // padded: the 16 rows of a tile hit distinct banks
-
-template <int R, int NM>
-struct CodesQ {
-  u32x4 c[NM][R];
-  uint32_t s[NM][R];
-};
-
 template <bool kPacked, int R, int NM>
 __device__ __forceinline__ void load_codes(CodesQ<R, NM>& st, const u32x4* const* pc,
                                            const uint16_t* const* ps, int s) {
@@ -318,72 +136,75 @@ __device__ __forceinline__ void load_codes(CodesQ<R, NM>& st, const u32x4* const
     }
 }
 
-// One super-step: codes from registers, B operands from LDS half h of the
-// staged chunk.
-template <int T, int R, int NM>
-__device__ __forceinline__ void compute_rows(const CodesQ<R, NM>& st, const u32x4* buf, int h,
+// One super-step: codes from registers, B operands from LDS (token rows of
+// kRow u32x4, `buf` at this super-step's first block).
+template <int T, int R, int NM, int kRow>
+__device__ __forceinline__ void compute_step(const CodesQ<R, NM>& st, const u32x4* buf,
                                              f32x4 (&acc)[NM][R][T], uint32_t magic) {
   const int lane = threadIdx.x & (kWave - 1);
   const int rA = lane & 15, gK = lane >> 4;
+  half2v s2[NM][R];
+#pragma unroll
+  for (int m = 0; m < NM; ++m)
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      _Float16 sh;
+      const uint16_t bits = (uint16_t)st.s[m][r];
+      __builtin_memcpy(&sh, &bits, 2);
+      s2[m][r] = half2v{sh, sh};
+    }
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     half8v b[T];
 #pragma unroll
-    for (int tt = 0; tt < T; ++tt) b[tt] = as_half8(buf[(tt * 16 + rA) * kLdsRowU4 + 16 * h + 4 * j + gK]);
+    for (int tt = 0; tt < T; ++tt) b[tt] = as_half8(buf[(tt * 16 + rA) * kRow + 4 * j + gK]);
 #pragma unroll
     for (int m = 0; m < NM; ++m)
 #pragma unroll
       for (int r = 0; r < R; ++r) {
-        _Float16 sh;
-        const uint16_t bits = (uint16_t)st.s[m][r];
-        __builtin_memcpy(&sh, &bits, 2);
-        const half2v s2 = {sh, sh};
-        const half8v a = q4_decode(st.c[m][r][j], s2, magic);
+        const half8v a = q4_decode(st.c[m][r][j], s2[m][r], magic);
 #pragma unroll
         for (int tt = 0; tt < T; ++tt) acc[m][r][tt] = mfma16(a, b[tt], acc[m][r][tt]);
       }
   }
 }
 
-template <int kMode, int T, int R, int W, bool kPacked>
-__device__ __forceinline__ void rows_pass_q(const FfnArgs& a, const Segment& seg, int t0, int r0,
-                                            int K, const uint8_t* C0, const uint8_t* C1,
-                                            const uint16_t* S0, const uint16_t* S1, u32x4* lds) {
+constexpr int gcd_c(int x, int y) { return y == 0 ? x : gcd_c(y, x % y); }
+constexpr int lcm_c(int x, int y) { return x / gcd_c(x, y) * y; }
+
+// One pass of a work item over T token tiles (tokens t0 .. t0 + 16 T - 1 of
+// the segment) and super-steps [lo, hi) of K.  The activations move through
+// LDS in chunks of C super-steps (one barrier per chunk); each thread keeps
+// the activations of the next A chunks and each wave the codes of the next
+// D - 1 super-steps in flight in registers.
+template <int kMode, int T, int R, int D, int A, int C, bool kPacked>
+__device__ __forceinline__ void q4_pass(const FfnArgs& a, const Segment& seg, int t0, int r0,
+                                        int q, int lo, int hi, int K, const uint8_t* C0,
+                                        const uint8_t* C1, const uint16_t* S0,
+                                        const uint16_t* S1, u32x4* lds) {
   constexpr int NM = kMode == 0 ? 2 : 1;
-  constexpr int kBuf = T * 16 * kLdsRowU4;       // u32x4 per LDS buffer
-  constexpr int kStg = T * 16 * kChunkU4 / (W * kWave);  // staged u32x4 per thread
+  constexpr int kRow = 16 * C + 1;      // u32x4 per token row of a chunk (+ pad)
+  constexpr int kBuf = T * 16 * kRow;   // u32x4 per LDS buffer
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
   const int wave = wave_id();
   const int rA = lane & 15, gK = lane >> 4;
-  const int nss = K / 128, nch = (nss + 1) / 2;
+  const int nss = K / 128;
   const int rw = r0 + wave * 16 * R;  // the wave's first row
 
-  // Staging map: thread item q covers token row tok, 16-byte block blk of the
-  // chunk (16 blocks per super-step).
+  // Staging: thread tid moves 16-byte block tid % 16 of token row
+  // tt * 16 + tid / 16 of each super-step (256 threads, one row block each).
   const uint16_t* X = static_cast<const uint16_t*>(kMode == 0 ? a.x16 : a.hh);
   const int ldx = kMode == 0 ? a.H : a.ldh;
-  const u32x4* xs[kStg];
-  int ld_off[kStg], blk_h[kStg], blk_l[kStg];
+  const u32x4* xs[T];
+  int ldo[T];
 #pragma unroll
-  for (int q = 0; q < kStg; ++q) {
-    const int idx = tid + q * W * kWave;
-    const int tok = idx / kChunkU4, blk = idx % kChunkU4;
+  for (int tt = 0; tt < T; ++tt) {
+    const int tok = tt * 16 + (tid >> 4);
     const int t = min(t0 + tok, seg.n - 1);
-    xs[q] = reinterpret_cast<const u32x4*>(X + (size_t)x_row(a, kMode, seg, t) * ldx);
-    ld_off[q] = tok * kLdsRowU4 + blk;
-    blk_h[q] = blk >> 4;
-    blk_l[q] = blk & 15;
+    xs[tt] = reinterpret_cast<const u32x4*>(X + (size_t)x_row(a, kMode, seg, t) * ldx) + (tid & 15);
+    ldo[tt] = tok * kRow + (tid & 15);
   }
-  // Chunk c holds super-steps 2c and 2c + 1 (the latter clamped to the last).
-  auto load_stage = [&](u32x4 (&v)[kStg], int c) {
-#pragma unroll
-    for (int q = 0; q < kStg; ++q) v[q] = xs[q][16 * min(2 * c + blk_h[q], nss - 1) + blk_l[q]];
-  };
-  auto store_stage = [&](const u32x4 (&v)[kStg], u32x4* buf) {
-#pragma unroll
-    for (int q = 0; q < kStg; ++q) buf[ld_off[q]] = v[q];
-  };
 
   const u32x4* pc[NM * R];
   const uint16_t* ps[NM * R];
@@ -417,27 +238,62 @@ __device__ __forceinline__ void rows_pass_q(const FfnArgs& a, const Segment& seg
       for (int tt = 0; tt < T; ++tt) acc[m][r][tt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   const uint32_t magic = opaque(0x64006400u);
-  u32x4 stg[kStg];
-  CodesQ<R, NM> cA, cB;
-  load_stage(stg, 0);
-  load_codes<kPacked>(cA, pc, ps, 0);
-  store_stage(stg, lds);
+  // The vector-memory counter completes loads in issue order, so a wait for
+  // one load also waits for every older one.  A chunk's activations are
+  // requested before the codes of the same step: waiting at the end of
+  // chunk c for the activations of chunk c + 1 then forces no codes that
+  // are not already due (needs D - 2 <= A C).
+  static_assert(D - 2 <= A * C, "activation ring too short for the code ring");
+  constexpr int U = lcm_c(D, A * C);  // steps of one loop turn: both rings wrap
+  CodesQ<R, NM> ring[D];
+  u32x4 stg[A][C][T];
+  // Prologue.  Indices past the range reload the last valid super-step, so
+  // every load is unconditional and the compiler's wait counts stay exact.
+#pragma unroll
+  for (int g = 0; g < A; ++g)
+#pragma unroll
+    for (int cs = 0; cs < C; ++cs)
+#pragma unroll
+      for (int tt = 0; tt < T; ++tt) stg[g][cs][tt] = xs[tt][16 * min(lo + g * C + cs, hi - 1)];
+#pragma unroll
+  for (int d = 0; d < D - 1; ++d) load_codes<kPacked>(ring[d], pc, ps, min(lo + d, hi - 1));
+#pragma unroll
+  for (int cs = 0; cs < C; ++cs)
+#pragma unroll
+    for (int tt = 0; tt < T; ++tt) lds[ldo[tt] + 16 * cs] = stg[0][cs][tt];
   __syncthreads();
-  for (int c = 0; c < nch; ++c) {
-    const u32x4* buf = lds + (c & 1) * kBuf;
-    load_stage(stg, min(c + 1, nch - 1));
-    load_codes<kPacked>(cB, pc, ps, min(2 * c + 1, nss - 1));
-    pipe_barrier();
-    compute_rows(cA, buf, 0, acc, magic);
-    load_codes<kPacked>(cA, pc, ps, min(2 * c + 2, nss - 1));
-    pipe_barrier();
-    if (2 * c + 1 < nss) compute_rows(cB, buf, 1, acc, magic);
-    // The other buffer was last read in chunk c - 1, before the barrier that
-    // ended it.
-    store_stage(stg, lds + ((c + 1) & 1) * kBuf);
-    __syncthreads();
+  for (int base = lo; base < hi; base += U) {
+#pragma unroll
+    for (int d = 0; d < U; ++d) {
+      const int s = base + d;
+      const int ch = (s - lo) / C;  // chunk of step s (d / C within the turn)
+      if (d % C == 0) {
+        // Request the activations of chunk ch + A into the slot chunk ch
+        // held (staged into LDS at the end of chunk ch - 1).
+#pragma unroll
+        for (int cs = 0; cs < C; ++cs)
+#pragma unroll
+          for (int tt = 0; tt < T; ++tt)
+            stg[(d / C) % A][cs][tt] = xs[tt][16 * min(s + A * C + cs, hi - 1)];
+      }
+      load_codes<kPacked>(ring[(d + D - 1) % D], pc, ps, min(s + D - 1, hi - 1));
+      pipe_barrier();
+      if (s < hi)
+        compute_step<T, R, NM, kRow>(ring[d % D], lds + (ch & 1) * kBuf + 16 * (d % C), acc, magic);
+      if (d % C == C - 1) {
+        // The other buffer was last read in chunk ch - 1, before the barrier
+        // that ended it.
+#pragma unroll
+        for (int cs = 0; cs < C; ++cs)
+#pragma unroll
+          for (int tt = 0; tt < T; ++tt)
+            lds[((ch + 1) & 1) * kBuf + ldo[tt] + 16 * cs] = stg[(d / C + 1) % A][cs][tt];
+        __syncthreads();
+      }
+    }
   }
 
+  // Lane holds D[row][token] for token rA of each tile and rows 4 gK + i.
 #pragma unroll
   for (int tt = 0; tt < T; ++tt) {
     const int t = t0 + tt * 16 + rA;
@@ -453,7 +309,9 @@ __device__ __forceinline__ void rows_pass_q(const FfnArgs& a, const Segment& seg
               (_Float16)(silu(acc[0][r][tt][i]) * acc[NM - 1][r][tt][i]);
         }
     } else {
-      float* dst = a.out + (size_t)out_row(a, seg, t) * a.H;
+      const size_t rows_out = (size_t)a.B * a.k + (size_t)a.S * a.B;
+      float* base_out = q == 0 ? a.out : a.part + (size_t)(q - 1) * rows_out * a.H;
+      float* dst = base_out + (size_t)out_row(a, seg, t) * a.H;
 #pragma unroll
       for (int r = 0; r < R; ++r)
         *reinterpret_cast<f32x4*>(dst + rw + 16 * r + 4 * gK) = acc[0][r][tt];
@@ -461,40 +319,109 @@ __device__ __forceinline__ void rows_pass_q(const FfnArgs& a, const Segment& seg
   }
 }
 
-template <int kMode, int R, int W, bool kPacked>
-__global__ __launch_bounds__(W * 64) void ffn_q4_rows_kernel(FfnArgs a) {
-  // Row counts are multiples of 128, so a workgroup's rows must divide 128.
-  static_assert(128 % (16 * R * W) == 0, "rows per workgroup must divide 128");
-  constexpr int NM = kMode == 0 ? 2 : 1;
-  __shared__ u32x4 lds[2 * 2 * 16 * kLdsRowU4];
-  Segment seg;
-  int unit;
-  if (!resolve_block(a, kMode, 16 * R * W, &seg, &unit)) return;
-  const int r0 = unit * 16 * R * W;
-  const int rows = kMode == 0 ? (seg.shared ? a.Fs : a.F) : a.H;
-  const int K = kMode == 0 ? a.H : (seg.shared ? a.Fs : a.F);
-  const size_t mat = (size_t)rows * K;
-  const void *M0, *M1, *Q0, *Q1;
-  if (kMode == 0) {
-    M0 = seg.shared ? a.sh_gate : a.gate;
-    M1 = seg.shared ? a.sh_up : a.up;
-    Q0 = seg.shared ? a.sh_gate_s : a.gate_s;
-    Q1 = seg.shared ? a.sh_up_s : a.up_s;
+// Work item `item` of a launch whose items cover 16 R kW rows over one of Q K
+// parts: shared experts first, then the activated routed experts in uniq
+// order.  False once the items of the activated experts are exhausted.
+__device__ __forceinline__ bool resolve_item(const FfnArgs& a, int mode, int rows_per_item,
+                                             int Q, int n_act, int item, Segment* seg, int* rb,
+                                             int* q) {
+  const int rows_r = mode == 0 ? a.F : a.H;
+  const int rows_s = mode == 0 ? a.Fs : a.H;
+  const int per_s = a.S > 0 ? rows_s / rows_per_item * Q : 0;
+  const int per_r = rows_r / rows_per_item * Q;
+  int rem;
+  if (item < a.S * per_s) {
+    seg->shared = true;
+    seg->id = item / per_s;
+    rem = item % per_s;
+    seg->n = a.B;
+    seg->base = a.B * a.k + seg->id * a.B;
   } else {
-    M0 = M1 = seg.shared ? a.sh_down : a.down;
-    Q0 = Q1 = seg.shared ? a.sh_down_s : a.down_s;
+    item -= a.S * per_s;
+    const int u = item / per_r;
+    if (u >= n_act) return false;
+    rem = item % per_r;
+    // The routing arrays come from the gating step; values outside their
+    // ranges (routing never computed) make the item empty instead of
+    // faulting.
+    const int e = a.uniq[u];
+    seg->shared = false;
+    seg->id = e;
+    if (e < 0 || e >= a.E) {
+      seg->n = 0;
+    } else {
+      seg->n = a.count[e];
+      seg->base = a.offset[e];
+      if (seg->n < 0 || seg->base < 0 || seg->base + seg->n > a.B * a.k) seg->n = 0;
+    }
   }
-  const uint8_t* C0 = static_cast<const uint8_t*>(M0) + seg.id * (mat / 2);
-  const uint8_t* C1 = static_cast<const uint8_t*>(M1) + seg.id * (mat / 2);
-  const uint16_t* S0 = static_cast<const uint16_t*>(Q0) + seg.id * (mat / 32);
-  const uint16_t* S1 = static_cast<const uint16_t*>(Q1) + seg.id * (mat / 32);
-  for (int t0 = 0; t0 < seg.n; t0 += 32) {
-    if (seg.n - t0 > 16)
-      rows_pass_q<kMode, 2, R, W, kPacked>(a, seg, t0, r0, K, C0, C1, S0, S1, lds);
-    else
-      rows_pass_q<kMode, 1, R, W, kPacked>(a, seg, t0, r0, K, C0, C1, S0, S1, lds);
+  *rb = rem / Q;
+  *q = rem % Q;
+  return true;
+}
+
+template <int kMode, int TMAX, int R, int D, int A, int C, bool kPacked>
+__global__ __launch_bounds__(kW * 64) void ffn_q4_kernel(FfnArgs a) {
+  __shared__ u32x4 lds[2 * TMAX * 16 * (16 * C + 1)];
+  constexpr int kRows = 16 * R * kW;
+  const int Q = kMode == 0 ? 1 : a.qparts;
+  const int n_act = min(*a.n_uniq, min(a.E, a.B * a.k));
+  const int rows_r = kMode == 0 ? a.F : a.H;
+  const int rows_s = kMode == 0 ? a.Fs : a.H;
+  const int n_items = (a.S > 0 ? a.S * (rows_s / kRows) : 0) * Q + max(n_act, 0) * (rows_r / kRows) * Q;
+  for (int item = blockIdx.x; item < n_items; item += gridDim.x) {
+    Segment seg;
+    int rb, q;
+    if (!resolve_item(a, kMode, kRows, Q, n_act, item, &seg, &rb, &q)) break;
+    if (seg.n <= 0) continue;
+    const int r0 = rb * kRows;
+    const int rows = kMode == 0 ? (seg.shared ? a.Fs : a.F) : a.H;
+    const int K = kMode == 0 ? a.H : (seg.shared ? a.Fs : a.F);
+    const int nss = K / 128;
+    const int lo = q * nss / Q, hi = (q + 1) * nss / Q;
+    if (hi <= lo) continue;  // the host keeps Q <= K / 128, so never taken
+    const size_t mat = (size_t)rows * K;
+    const void *M0, *M1, *Q0, *Q1;
+    if (kMode == 0) {
+      M0 = seg.shared ? a.sh_gate : a.gate;
+      M1 = seg.shared ? a.sh_up : a.up;
+      Q0 = seg.shared ? a.sh_gate_s : a.gate_s;
+      Q1 = seg.shared ? a.sh_up_s : a.up_s;
+    } else {
+      M0 = M1 = seg.shared ? a.sh_down : a.down;
+      Q0 = Q1 = seg.shared ? a.sh_down_s : a.down_s;
+    }
+    const uint8_t* C0 = static_cast<const uint8_t*>(M0) + seg.id * (mat / 2);
+    const uint8_t* C1 = static_cast<const uint8_t*>(M1) + seg.id * (mat / 2);
+    const uint16_t* S0 = static_cast<const uint16_t*>(Q0) + seg.id * (mat / 32);
+    const uint16_t* S1 = static_cast<const uint16_t*>(Q1) + seg.id * (mat / 32);
+    for (int t0 = 0; t0 < seg.n; t0 += 16 * TMAX) {
+      const int T = min(TMAX, (seg.n - t0 + 15) / 16);
+      if (TMAX >= 4 && T >= 4)
+        q4_pass<kMode, (TMAX >= 4 ? 4 : 1), R, D, A, C, kPacked>(a, seg, t0, r0, q, lo, hi, K, C0, C1, S0, S1, lds);
+      else if (TMAX >= 3 && T == 3)
+        q4_pass<kMode, (TMAX >= 3 ? 3 : 1), R, D, A, C, kPacked>(a, seg, t0, r0, q, lo, hi, K, C0, C1, S0, S1, lds);
+      else if (TMAX >= 2 && T == 2)
+        q4_pass<kMode, (TMAX >= 2 ? 2 : 1), R, D, A, C, kPacked>(a, seg, t0, r0, q, lo, hi, K, C0, C1, S0, S1, lds);
+      else
+        q4_pass<kMode, 1, R, D, A, C, kPacked>(a, seg, t0, r0, q, lo, hi, K, C0, C1, S0, S1, lds);
+    }
   }
-  (void)NM;
+}
+
+// expert_out += the partial sums of K parts 1 .. Q - 1, added in part order.
+__global__ __launch_bounds__(256) void q4_reduce_kernel(float* __restrict__ out,
+                                                        const float* __restrict__ part, int Q,
+                                                        size_t n4) {
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n4) return;
+  f32x4 v = reinterpret_cast<const f32x4*>(out)[i];
+  for (int q = 1; q < Q; ++q) {
+    const f32x4 p = reinterpret_cast<const f32x4*>(part)[(size_t)(q - 1) * n4 + i];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) v[c] += p[c];
+  }
+  reinterpret_cast<f32x4*>(out)[i] = v;
 }
 
 // x [B, H] bf16 -> x16 [B, H] fp16 in the kernels' order (block_pos, then
@@ -518,39 +445,6 @@ __global__ __launch_bounds__(256) void q4_prep_x_kernel(const uint16_t* __restri
   reinterpret_cast<u32x4*>(x16)[block_pos(i)] = r;
 }
 
-#ifndef S2MOE_Q4_STEPS_PER_WAVE
-#define S2MOE_Q4_STEPS_PER_WAVE 8
-#endif
-
-int pick_waves_q4(int nss, int tiles) {
-  int w = 1;
-  while (w * 2 <= 8 && nss / (w * 2) >= S2MOE_Q4_STEPS_PER_WAVE && (w * 2) * tiles <= 32)
-    w *= 2;
-  return w;
-}
-
-template <int kMode, int TMAX, int R, bool kPacked>
-hipError_t launch_q4_mode_p(const FfnArgs& a, hipStream_t s) {
-  const int nm = kMode == 0 ? 2 : 1;
-  int nss = kMode == 0 ? a.H / 128 : a.F / 128;
-  if (kMode == 1 && a.S > 0) nss = min(nss, a.Fs / 128);
-  const int w = pick_waves_q4(nss, nm * R * TMAX);
-  const dim3 grid(n_blocks(a, kMode, 16 * R));
-  switch (w) {
-    case 1: hipLaunchKernelGGL((ffn_q4_kernel<kMode, TMAX, R, 1, kPacked>), grid, dim3(64), 0, s, a); break;
-    case 2: hipLaunchKernelGGL((ffn_q4_kernel<kMode, TMAX, R, 2, kPacked>), grid, dim3(128), 0, s, a); break;
-    case 4: hipLaunchKernelGGL((ffn_q4_kernel<kMode, TMAX, R, 4, kPacked>), grid, dim3(256), 0, s, a); break;
-    default: hipLaunchKernelGGL((ffn_q4_kernel<kMode, TMAX, R, 8, kPacked>), grid, dim3(512), 0, s, a); break;
-  }
-  return hipGetLastError();
-}
-
-template <int kMode, int TMAX, int R>
-hipError_t launch_q4_mode(const FfnArgs& a, hipStream_t s) {
-  return a.packed ? launch_q4_mode_p<kMode, TMAX, R, true>(a, s)
-                  : launch_q4_mode_p<kMode, TMAX, R, false>(a, s);
-}
-
 // Compute units of the current device, queried once per device.
 hipError_t device_cus(int* cus) {
   static std::atomic<int> cache[64];
@@ -565,45 +459,70 @@ hipError_t device_cus(int* cus) {
   return hipSuccess;
 }
 
-template <int kMode, int R, int W>
-hipError_t launch_q4_rows(const FfnArgs& a, hipStream_t s) {
-  const dim3 grid(n_blocks(a, kMode, 16 * R * W));
-  if (a.packed)
-    hipLaunchKernelGGL((ffn_q4_rows_kernel<kMode, R, W, true>), grid, dim3(W * 64), 0, s, a);
-  else
-    hipLaunchKernelGGL((ffn_q4_rows_kernel<kMode, R, W, false>), grid, dim3(W * 64), 0, s, a);
+// Workgroups of one kernel that fit on a compute unit at once, queried once
+// per kernel (the same on every device of one type).
+template <class Kern>
+hipError_t resident_per_cu(Kern kern, int* n) {
+  static std::atomic<int> cache{0};
+  if ((*n = cache.load(std::memory_order_relaxed)) > 0) return hipSuccess;
+  hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(n, kern, kW * 64, 0);
+  if (e != hipSuccess) return e;
+  if (*n < 1) *n = 1;
+  cache.store(*n, std::memory_order_relaxed);
+  return hipSuccess;
+}
+
+// Launch of one projection: the grid holds every work item a batch could
+// have (all min(E, B k) routed slots active), capped at the workgroups the
+// GPU holds at once.
+template <int kMode, int TMAX, int R, int D, int A, int C, bool kPacked>
+hipError_t launch_q4(const FfnArgs& a, int Q, hipStream_t s) {
+  auto kern = ffn_q4_kernel<kMode, TMAX, R, D, A, C, kPacked>;
+  int cus = 0, per_cu = 0;
+  hipError_t err = device_cus(&cus);
+  if (err == hipSuccess) err = resident_per_cu(kern, &per_cu);
+  if (err != hipSuccess) return err;
+  constexpr int kRows = 16 * R * kW;
+  const int rows_r = kMode == 0 ? a.F : a.H;
+  const int rows_s = kMode == 0 ? a.Fs : a.H;
+  const int slots = min(a.E, a.B * a.k);
+  const long items = ((long)(a.S > 0 ? a.S * (rows_s / kRows) : 0) + (long)slots * (rows_r / kRows)) * Q;
+  const long grid = min(items, (long)cus * per_cu);
+  if (grid < 1) return hipSuccess;
+  hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(kW * 64), 0, s, a);
   return hipGetLastError();
 }
 
-// Tile choices per batch size.
-// - Gate-up above 8 tokens runs on the row-split kernel with one row tile
-//   per wave (64 rows per workgroup, activations shared through LDS, up to
-//   two token tiles per pass).  One row tile per wave keeps it at four
-//   waves per SIMD (two row tiles: two), and the finer work units leave a
-//   smaller partly filled last round of workgroups.
-// - Gate-up up to 8 tokens and down up to 16 tokens hold one token tile,
-//   and the row tiles per wave are the most (gate-up 2, down 4) that still
-//   give every compute unit a workgroup: with one or two activated experts
-//   (a draft step, or B = 1) fewer rows per workgroup spread the weight
-//   stream over the whole GPU.
-// - Down above 16 tokens holds two token tiles with 4 row tiles per wave.
-//   Buckets larger than 32 tokens take several passes over the same rows.
-hipError_t launch_q4_tiles(const FfnArgs& a, hipStream_t s) {
-  hipError_t err;
-  int cus = 0;
-  if (a.B > 8) {
-    err = launch_q4_rows<0, 1, 4>(a, s);
-  } else {
-    err = device_cus(&cus);
-    if (err != hipSuccess) return err;
-    err = n_blocks(a, 0, 32) >= cus ? launch_q4_mode<0, 1, 2>(a, s) : launch_q4_mode<0, 1, 1>(a, s);
-  }
+template <int kMode, int TMAX, int R, int D, int A, int C>
+hipError_t launch_q4_layout(const FfnArgs& a, int Q, hipStream_t s) {
+  return a.packed ? launch_q4<kMode, TMAX, R, D, A, C, true>(a, Q, s)
+                  : launch_q4<kMode, TMAX, R, D, A, C, false>(a, Q, s);
+}
+
+#ifndef S2MOE_Q4_RING
+#define S2MOE_Q4_RING 2
+#endif
+#ifndef S2MOE_Q4_ACT_RING
+#define S2MOE_Q4_ACT_RING 1
+#endif
+#ifndef S2MOE_Q4_CHUNK
+#define S2MOE_Q4_CHUNK 1
+#endif
+#ifndef S2MOE_Q4_GATEUP_R
+#define S2MOE_Q4_GATEUP_R 1
+#endif
+#ifndef S2MOE_Q4_DOWN_R
+#define S2MOE_Q4_DOWN_R 2
+#endif
+
+template <int TMAX>
+hipError_t launch_q4_pair(const FfnArgs& a, hipStream_t s) {
+  constexpr int D = S2MOE_Q4_RING;
+  static_assert(16 * S2MOE_Q4_DOWN_R * kW == kQ4DownRows, "down rows per item");
+  constexpr int A = S2MOE_Q4_ACT_RING, C = S2MOE_Q4_CHUNK;
+  hipError_t err = launch_q4_layout<0, TMAX, S2MOE_Q4_GATEUP_R, D, A, C>(a, 1, s);
   if (err != hipSuccess) return err;
-  if (a.B > 16) return launch_q4_mode<1, 2, 4>(a, s);
-  if (cus == 0 && (err = device_cus(&cus)) != hipSuccess) return err;
-  if (n_blocks(a, 1, 64) >= cus) return launch_q4_mode<1, 1, 4>(a, s);
-  if (n_blocks(a, 1, 32) >= cus) return launch_q4_mode<1, 1, 2>(a, s);
-  return launch_q4_mode<1, 1, 1>(a, s);
+  return launch_q4_layout<1, TMAX, S2MOE_Q4_DOWN_R, D, A, C>(a, a.qparts, s);
 }
 
 }  // namespace
@@ -612,8 +531,17 @@ hipError_t launch_ffn_q4(const FfnArgs& a, hipStream_t s) {
   const int n8 = a.B * a.H / 8;
   hipLaunchKernelGGL(q4_prep_x_kernel, dim3((n8 + 255) / 256), dim3(256), 0, s,
                      static_cast<const uint16_t*>(a.x), static_cast<uint16_t*>(a.x16), n8);
-  const hipError_t err = hipGetLastError();
-  return err != hipSuccess ? err : launch_q4_tiles(a, s);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return err;
+  // Token tiles held in one pass: the batch bounds every bucket.
+  if (a.B <= 16) err = launch_q4_pair<1>(a, s);
+  else if (a.B <= 32) err = launch_q4_pair<2>(a, s);
+  else err = launch_q4_pair<4>(a, s);
+  if (err != hipSuccess || a.qparts <= 1) return err;
+  const size_t n4 = ((size_t)a.B * a.k + (size_t)a.S * a.B) * a.H / 4;
+  hipLaunchKernelGGL(q4_reduce_kernel, dim3((unsigned)((n4 + 255) / 256)), dim3(256), 0, s, a.out,
+                     a.part, a.qparts, n4);
+  return hipGetLastError();
 }
 
 }  // namespace s2moe

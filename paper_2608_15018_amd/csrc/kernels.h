@@ -67,9 +67,31 @@ struct FfnArgs {
   void* hh;  // workspace: SwiGLU activations [B*k + S*B, ldh] (fp32, bf16 or fp16)
   int ldh;
   void* x16;  // workspace, int4 weights only: x as fp16 [B, H] in the kernels' order
+  float* part;  // workspace, int4 weights only: down partial sums of K parts 1..Q-1,
+                // [Q - 1][B*k + S*B][H] fp32 (unused when Q == 1)
+  int qparts;   // Q: K parts of the int4 down projection (q4_down_parts)
   bool packed;  // weights in the packed tile order (pack.hip)
   float* out;  // [B*k + S*B, H]
 };
+
+// int4 expert FFN: rows of one down-projection work item (8 row tiles), and
+// the number of K parts its reduction dimension is split into.  The parts
+// give a launch at least 1024 work items (four per compute unit of a 256-CU
+// GPU) when the batch activates few experts, up to 8 parts; each part spans
+// at least one 128-wide K super-step.  Host-side: the workspace size
+// depends on it.
+constexpr int kQ4DownRows = 128;
+
+inline int q4_down_parts(int B, int k, int E, int H, int F, int S, int Fs) {
+  const int slots = E < B * k ? E : B * k;
+  const int items = (S + slots) * (H / kQ4DownRows);
+  int q = (1024 + items - 1) / items;
+  int nss = F / 128;
+  if (S > 0 && Fs / 128 < nss) nss = Fs / 128;
+  if (q > 8) q = 8;
+  if (q > nss) q = nss;
+  return q < 1 ? 1 : q;
+}
 
 struct CombineArgs {
   const float* gate_w;
