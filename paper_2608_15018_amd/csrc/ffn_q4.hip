@@ -21,9 +21,10 @@
 // - A work item is 16 R W rows of one expert (W = 4 waves, R row tiles per
 //   wave) over one of Q contiguous K parts, for all tokens routed to that
 //   expert.  The launch has at most as many workgroups as fit on the GPU at
-//   once; each takes items blockIdx.x, + gridDim.x, ... until the activated
-//   experts' items run out.  (Measured on MI355X: dealing equal runs of
-//   consecutive items, or one workgroup per item, was 3-15 % slower.)
+//   once, a multiple of the 8 XCDs.  Each XCD takes a contiguous slice of
+//   the activated experts' items and deals it round-robin to its
+//   workgroups.  (Measured on MI355X: dealing equal runs of consecutive
+//   items, or one workgroup per item, was 3-15 % slower.)
 // - The waves of a workgroup stream different rows over the same K range, so
 //   they share the activations: the workgroup stages the tokens' next
 //   super-step in LDS while the current one is decoded (double-buffered, one
@@ -55,7 +56,11 @@ namespace {
 typedef _Float16 half2v __attribute__((ext_vector_type(2)));
 typedef _Float16 half8v __attribute__((ext_vector_type(8)));
 
-constexpr int kW = 4;  // waves per workgroup
+constexpr int kW = 4;     // waves per workgroup
+constexpr int kXcds = 8;  // accelerator dies of an MI355X, each with its own L2
+#ifndef S2MOE_Q4_XCD_SLICES
+#define S2MOE_Q4_XCD_SLICES 1
+#endif
 
 __device__ __forceinline__ f32x4 mfma16(half8v a, half8v b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
@@ -360,8 +365,12 @@ __device__ __forceinline__ bool resolve_item(const FfnArgs& a, int mode, int row
   return true;
 }
 
+#ifndef S2MOE_Q4_MINWAVES_T4
+#define S2MOE_Q4_MINWAVES_T4 2
+#endif
+
 template <int kMode, int TMAX, int R, int D, int A, int C, bool kPacked>
-__global__ __launch_bounds__(kW * 64) void ffn_q4_kernel(FfnArgs a) {
+__global__ __launch_bounds__(kW * 64, TMAX >= 4 ? S2MOE_Q4_MINWAVES_T4 : 1) void ffn_q4_kernel(FfnArgs a) {
   __shared__ u32x4 lds[2 * TMAX * 16 * (16 * C + 1)];
   constexpr int kRows = 16 * R * kW;
   const int Q = kMode == 0 ? 1 : a.qparts;
@@ -369,7 +378,19 @@ __global__ __launch_bounds__(kW * 64) void ffn_q4_kernel(FfnArgs a) {
   const int rows_r = kMode == 0 ? a.F : a.H;
   const int rows_s = kMode == 0 ? a.Fs : a.H;
   const int n_items = (a.S > 0 ? a.S * (rows_s / kRows) : 0) * Q + max(n_act, 0) * (rows_r / kRows) * Q;
+  // Workgroups are dealt to the XCDs round-robin (blockIdx % kXcds), each
+  // XCD with its own L2.  Each XCD takes one contiguous slice of the items
+  // (expert-major), dealt round-robin to its workgroups, so that an expert's
+  // activations are fetched into one or two L2s instead of all of them.
+  // Which XCD runs a workgroup affects only speed, never results.
+#if S2MOE_Q4_XCD_SLICES
+  const int xcd = blockIdx.x % kXcds, lw = blockIdx.x / kXcds, gx = gridDim.x / kXcds;
+  const int i_lo = (int)((long)n_items * xcd / kXcds);
+  const int i_hi = (int)((long)n_items * (xcd + 1) / kXcds);
+  for (int item = i_lo + lw; item < i_hi; item += gx) {
+#else
   for (int item = blockIdx.x; item < n_items; item += gridDim.x) {
+#endif
     Segment seg;
     int rb, q;
     if (!resolve_item(a, kMode, kRows, Q, n_act, item, &seg, &rb, &q)) break;
@@ -487,8 +508,9 @@ hipError_t launch_q4(const FfnArgs& a, int Q, hipStream_t s) {
   const int rows_s = kMode == 0 ? a.Fs : a.H;
   const int slots = min(a.E, a.B * a.k);
   const long items = ((long)(a.S > 0 ? a.S * (rows_s / kRows) : 0) + (long)slots * (rows_r / kRows)) * Q;
-  const long grid = min(items, (long)cus * per_cu);
-  if (grid < 1) return hipSuccess;
+  // A multiple of kXcds workgroups, so every XCD has the same number.
+  const long grid = (min(items + kXcds - 1, (long)cus * per_cu) / kXcds) * kXcds;
+  if (grid < kXcds) return hipSuccess;
   hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(kW * 64), 0, s, a);
   return hipGetLastError();
 }
@@ -507,6 +529,9 @@ hipError_t launch_q4_layout(const FfnArgs& a, int Q, hipStream_t s) {
 #endif
 #ifndef S2MOE_Q4_CHUNK
 #define S2MOE_Q4_CHUNK 1
+#endif
+#ifndef S2MOE_Q4_TMAX_LARGE
+#define S2MOE_Q4_TMAX_LARGE 4
 #endif
 #ifndef S2MOE_Q4_GATEUP_R
 #define S2MOE_Q4_GATEUP_R 1
@@ -536,7 +561,7 @@ hipError_t launch_ffn_q4(const FfnArgs& a, hipStream_t s) {
   // Token tiles held in one pass: the batch bounds every bucket.
   if (a.B <= 16) err = launch_q4_pair<1>(a, s);
   else if (a.B <= 32) err = launch_q4_pair<2>(a, s);
-  else err = launch_q4_pair<4>(a, s);
+  else err = launch_q4_pair<S2MOE_Q4_TMAX_LARGE>(a, s);
   if (err != hipSuccess || a.qparts <= 1) return err;
   const size_t n4 = ((size_t)a.B * a.k + (size_t)a.S * a.B) * a.H / 4;
   hipLaunchKernelGGL(q4_reduce_kernel, dim3((unsigned)((n4 + 255) / 256)), dim3(256), 0, s, a.out,

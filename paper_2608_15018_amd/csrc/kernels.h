@@ -76,16 +76,20 @@ struct FfnArgs {
 
 // int4 expert FFN: rows of one down-projection work item (8 row tiles), and
 // the number of K parts its reduction dimension is split into.  The parts
-// give a launch at least 1024 work items (four per compute unit of a 256-CU
-// GPU) when the batch activates few experts, up to 8 parts; each part spans
-// at least one 128-wide K super-step.  Host-side: the workspace size
-// depends on it.
+// give a launch at least 256 work items (one per compute unit of a 256-CU
+// GPU) when the batch activates so few experts that it would have fewer, up
+// to 8 parts; each part spans at least one 128-wide K super-step.  (Targets
+// of 512 to 2048 items measured the same within 4 % on MI355X, and cost
+// partial-sum traffic.)  Host-side: the workspace size depends on it.
 constexpr int kQ4DownRows = 128;
+#ifndef S2MOE_Q4_DOWN_ITEMS
+#define S2MOE_Q4_DOWN_ITEMS 256
+#endif
 
 inline int q4_down_parts(int B, int k, int E, int H, int F, int S, int Fs) {
   const int slots = E < B * k ? E : B * k;
   const int items = (S + slots) * (H / kQ4DownRows);
-  int q = (1024 + items - 1) / items;
+  int q = (S2MOE_Q4_DOWN_ITEMS + items - 1) / items;
   int nss = F / 128;
   if (S > 0 && Fs / 128 < nss) nss = Fs / 128;
   if (q > 8) q = 8;
