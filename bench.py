@@ -531,71 +531,68 @@ def bench_stack(args, wl, shape, B: int, wid: int) -> int:
     return 0
 
 
-def main(argv=None):
-    ap = argparse.ArgumentParser()
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="c2",
-                    choices=["c1", "c2", "c3", "c4", "c5", "t_qwen3", "t_deepseek", "t_olmoe",
-                             "t_gptoss", "d_olmoe", "d_deepseek", "d_qwen3", "d_gptoss"],
-                    help="c*: verify-MoE layer; t_*: draft-tree expansion (s2moe_expand); "
-                         "d_*: expert-sparse draft step over a model's MoE layers")
-    ap.add_argument("--wdt", default="bf16", choices=["bf16", "q4g32"],
-                    help="d_* workloads: expert weight format")
-    ap.add_argument("--trees", type=int, default=256,
-                    help="t_* workloads: draft trees per s2moe_expand launch")
-    ap.add_argument("--batch", type=int, default=None, help="draft tokens (default: workload's)")
-    ap.add_argument("--alpha", type=float, default=None)
-    ap.add_argument("--seed", type=int, default=1)
-    ap.add_argument("--layers", type=int, default=1,
-                    help="c*: verify this many layers of the workload back to back, each with its "
-                         "own router, hidden states, confidences and expert weights (c5: up to 24)")
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--plain-weights", action="store_true",
-                    help="stream the row-major weights instead of the packed tile order")
-    ap.add_argument("--copy-probe", action="store_true",
-                    help="only run a plain device copy of 1 GiB (calibrates HBM byte counters)")
-    ap.add_argument("--no-scrub", action="store_true",
-                    help="time repeated launches on one copy of the inputs (cache-resident "
-                         "when small) instead of cycling through copies larger than the caches")
-    args = ap.parse_args(argv)
+def stream_read_gbs() -> float:
+    """GB/s of s2moe_stream_read over 2 GiB (5 passes between one event pair)."""
+    import torch
 
-    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU only: the verify-MoE path here runs on a single "
-              "MI355X (no multi-GPU path is built); run it with --gpus 1.", file=sys.stderr)
-        return 2
+    import paper_2608_15018_amd as s2
+    stream = torch.cuda.current_stream()
+    buf = torch.ones(1 << 29, dtype=torch.float32, device="cuda")
+    sink = torch.empty(s2.STREAM_SINK_WORDS, dtype=torch.int32, device="cuda")
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    s2.stream_read(buf, sink)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(5):
+        s2.stream_read(buf, sink)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    gbs = 5 * buf.numel() * 4 / (e0.elapsed_time(e1) / 1e3) / 1e9
+    del buf, sink
+    return gbs
 
+
+# Extra single-GPU configurations measured by the default run beside the
+# headline workload: the Mixtral-shaped int4-g32 layer at 16 and 64 draft
+# tokens (layer 0 of the 24-layer stack).
+EXTRA_CONFIGS = (("c5", 16), ("c5", 64))
+
+
+def extra_configs(args) -> dict:
+    """FFN roofline of each EXTRA_CONFIGS workload, timed in this run."""
+    import gc
+
+    import torch
+
+    from synth.configs import WORKLOAD_ID, WORKLOADS
+    res = {}
+    for name, B in EXTRA_CONFIGS:
+        wl = WORKLOADS[name]
+        default_B = wl.batches[-1 if name == "c5" else 0]
+        o = bench_layer(args, wl, wl.shape, B, default_B, WORKLOAD_ID[name], stream_ref=False,
+                        cpu_baseline=False)
+        r = o["roofline"]
+        res[f"{name}_b{B}"] = {
+            "workload": o["config"]["workload"], "draft_tokens": B, "n_uniq": o["n_uniq"],
+            "dtype": o["dtype"], "ms_per_step": o["ms_per_step"],
+            "draft_tokens_per_s": o["value"], "ffn_avg_launch_us": r["avg_launch_us"],
+            "achieved_gbs": r["achieved"], "frac": r["frac"], "traffic": r["traffic"],
+            "bytes_per_launch": r["bytes_per_launch"], "ffn_timing": o["ffn_timing"]}
+        _log(f"[bench] extra {name} B={B}: {r['achieved']:.0f} GB/s ({r['frac']:.3f} of peak)")
+        gc.collect()
+        torch.cuda.empty_cache()
+    return res
+
+
+def bench_layer(args, wl, shape, B: int, default_B: int, wid: int, stream_ref: bool = True,
+                cpu_baseline: bool = True) -> dict:
+    """One verify-MoE layer (layer 0 of the workload) at B draft tokens: whole
+    steps timed on the host, the expert-FFN calls timed with HIP events, the
+    read-stream reference and the oracle on the host cores."""
     import torch
 
     import paper_2608_15018_amd as s2
     from synth import gen
-    from synth.configs import WORKLOAD_ID, WORKLOADS
-
-    torch.cuda.set_device(0)
-    if args.copy_probe:
-        # A plain copy of known size: each launch reads and writes 1 GiB.
-        n = 1 << 30
-        src = torch.ones(n // 4, dtype=torch.float32, device="cuda")
-        dst = torch.empty_like(src)
-        for _ in range(5):
-            dst.copy_(src)
-        torch.cuda.synchronize()
-        print(json.dumps({"copy_probe_bytes_read": n, "copy_probe_bytes_written": n,
-                          "launches": 5}))
-        return 0
-    s2.load()
-    if args.workload.startswith("t_"):
-        return bench_expand(args)
-    if args.workload.startswith("d_"):
-        return bench_draft(args)
-    wl = WORKLOADS[args.workload]
-    shape = wl.shape if args.alpha is None else wl.shape.with_(alpha=args.alpha)
-    default_B = wl.batches[-1 if args.workload == "c5" else 0]
-    B = args.batch or default_B
-    wid = WORKLOAD_ID[wl.name]
-    if args.layers > 1:
-        return bench_stack(args, wl, shape, B, wid)
 
     t0 = time.time()
     router = gen.make_router(shape, args.seed, 0, wid, wl.router_std)
@@ -661,23 +658,13 @@ def main(argv=None):
 
     # Reference: a plain sequential read of 2 GiB with the FFN's load type
     # (s2moe_stream_read, a diagnostic of the library).
-    buf = torch.ones(1 << 29, dtype=torch.float32, device="cuda")
-    sink = torch.empty(s2.STREAM_SINK_WORDS, dtype=torch.int32, device="cuda")
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    s2.stream_read(buf, sink)
-    torch.cuda.synchronize()
-    e0.record(stream)
-    for _ in range(5):
-        s2.stream_read(buf, sink)
-    e1.record(stream)
-    torch.cuda.synchronize()
-    stream_gbs = 5 * buf.numel() * 4 / (e0.elapsed_time(e1) / 1e3) / 1e9
-    del buf, sink
-
+    stream_gbs = None
+    if stream_ref:
+        stream_gbs = stream_read_gbs()
     ffn_note = (f"one event pair around {args.steps} back-to-back calls over {copies} "
                 f"weight cop{'y' if copies == 1 else 'ies'}")
     cpu = None
-    if not args.no_cpu_baseline:
+    if cpu_baseline and not args.no_cpu_baseline:
         import oracle
         try:
             from threadpoolctl import threadpool_info
@@ -718,11 +705,86 @@ def main(argv=None):
         "n_uniq": n_uniq,
         "reuse_ratio": n_uniq / (B * shape.top_k),
         "ffn_timing": ffn_note,
-        "stream_read": {"value": stream_gbs, "unit": "GB/s",
-                        "kind": "s2moe_stream_read: one sequential pass over 2 GiB, 16-byte "
-                                "nontemporal loads",
-                        "ffn_frac_of_stream": achieved / stream_gbs},
     }
+    if stream_gbs is not None:
+        out["stream_read"] = {"value": stream_gbs, "unit": "GB/s",
+                              "kind": "s2moe_stream_read: one sequential pass over 2 GiB, "
+                                      "16-byte nontemporal loads",
+                              "ffn_frac_of_stream": achieved / stream_gbs}
+    return out
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="c2",
+                    choices=["c1", "c2", "c3", "c4", "c5", "t_qwen3", "t_deepseek", "t_olmoe",
+                             "t_gptoss", "d_olmoe", "d_deepseek", "d_qwen3", "d_gptoss"],
+                    help="c*: verify-MoE layer; t_*: draft-tree expansion (s2moe_expand); "
+                         "d_*: expert-sparse draft step over a model's MoE layers")
+    ap.add_argument("--wdt", default="bf16", choices=["bf16", "q4g32"],
+                    help="d_* workloads: expert weight format")
+    ap.add_argument("--trees", type=int, default=256,
+                    help="t_* workloads: draft trees per s2moe_expand launch")
+    ap.add_argument("--batch", type=int, default=None, help="draft tokens (default: workload's)")
+    ap.add_argument("--alpha", type=float, default=None)
+    ap.add_argument("--seed", type=int, default=1)
+    ap.add_argument("--layers", type=int, default=1,
+                    help="c*: verify this many layers of the workload back to back, each with its "
+                         "own router, hidden states, confidences and expert weights (c5: up to 24)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extra", action="store_true",
+                    help="default run: skip the extra int4 configurations (c5 at B=16 and 64)")
+    ap.add_argument("--plain-weights", action="store_true",
+                    help="stream the row-major weights instead of the packed tile order")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="only run a plain device copy of 1 GiB (calibrates HBM byte counters)")
+    ap.add_argument("--no-scrub", action="store_true",
+                    help="time repeated launches on one copy of the inputs (cache-resident "
+                         "when small) instead of cycling through copies larger than the caches")
+    args = ap.parse_args(argv)
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the verify-MoE path here runs on a single "
+              "MI355X (no multi-GPU path is built); run it with --gpus 1.", file=sys.stderr)
+        return 2
+
+    import torch
+
+    import paper_2608_15018_amd as s2
+    from synth import gen
+    from synth.configs import WORKLOAD_ID, WORKLOADS
+
+    torch.cuda.set_device(0)
+    if args.copy_probe:
+        # A plain copy of known size: each launch reads and writes 1 GiB.
+        n = 1 << 30
+        src = torch.ones(n // 4, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_probe_bytes_read": n, "copy_probe_bytes_written": n,
+                          "launches": 5}))
+        return 0
+    s2.load()
+    if args.workload.startswith("t_"):
+        return bench_expand(args)
+    if args.workload.startswith("d_"):
+        return bench_draft(args)
+    wl = WORKLOADS[args.workload]
+    shape = wl.shape if args.alpha is None else wl.shape.with_(alpha=args.alpha)
+    default_B = wl.batches[-1 if args.workload == "c5" else 0]
+    B = args.batch or default_B
+    wid = WORKLOAD_ID[wl.name]
+    if args.layers > 1:
+        return bench_stack(args, wl, shape, B, wid)
+
+    out = bench_layer(args, wl, shape, B, default_B, wid)
+    if not args.no_extra and args.workload == "c2" and args.batch is None and args.alpha is None:
+        out["extra_configs"] = extra_configs(args)
     print(json.dumps(out), flush=True)
     return 0
 

@@ -10,10 +10,12 @@ activates some |U| experts -- and fits t0 and T_exp by least squares.
 
     python -m paper_2608_15018_amd.calibrate --workload c2 [--out file.json]
 
-Timing: per configuration, `steps` passes after one warm-up pass, each
-timed with HIP events on the launch stream after a 512 MiB write that
-evicts the caches; the median is used.  Two latencies are fitted: the whole
-pass (route -> gate -> experts -> combine) and the expert-FFN call alone.
+Timing: per configuration, `steps` back-to-back passes between one pair of
+HIP events on the launch stream, cycling through copies of the expert
+weights large enough that the last-level cache cannot serve a pass from the
+previous one (the protocol of bench.py); the average is used.  Two
+latencies are fitted: the whole pass (route -> gate -> experts -> combine)
+and the expert-FFN call alone.
 """
 
 from __future__ import annotations
@@ -42,63 +44,114 @@ def fit_linear(u, t) -> dict:
             "n": int(u.size)}
 
 
-def measure(workload: str, batches, alphas, seeds, steps: int = 20, device="cuda") -> list:
-    """One sample per (B, alpha, seed): |U| and median step / FFN latency (us)."""
+# Timed passes cycle through copies of the expert weights that together
+# exceed this many bytes, so that the 256 MB last-level cache cannot serve a
+# pass from the previous one (the protocol of bench.py).
+ROTATE_BYTES = 600_000_000
+
+
+def expert_bytes(shape, F: int) -> int:
+    """HBM bytes of one expert's gate, up and down weights (int4 scales included)."""
+    n = 3 * F * shape.hidden
+    if shape.wdt == "bf16":
+        return 2 * n
+    if shape.wdt == "f32":
+        return 4 * n
+    return n // 2 + 2 * (n // 32)
+
+
+def sample_inputs(wl, shape, B: int, seed: int, reject_for=None):
+    """Router, hidden states and confidences of one sample.  `reject_for`,
+    if given, maps the router to a synth.gen.make_batch rejection callback
+    (tokens to redraw), e.g. one that keeps every ranking decision clear of
+    ties."""
+    from synth import gen  # the repository root is on sys.path (run from there)
+    from synth.configs import WORKLOAD_ID
+
+    wid = WORKLOAD_ID[wl.name]
+    router = gen.make_router(shape, seed, 0, wid, wl.router_std)
+    reject = reject_for(router) if reject_for is not None else None
+    x, conf_w, _ = gen.make_batch(shape, B, seed, 0, wid, wl.rho, reject)
+    return router, x, conf_w
+
+
+def measure(workload: str, batches, alphas, seeds, steps: int = 20, device="cuda",
+            shape=None, reject_for=None, rotate_bytes: int = ROTATE_BYTES) -> list:
+    """One sample per (B, alpha, seed): |U| and the average latency (us) of a
+    whole pass (route -> gate -> experts -> combine) and of the expert-FFN
+    call alone.  Each latency is `steps` back-to-back passes between one pair
+    of HIP events on the launch stream, cycling through copies of the expert
+    weights (at least `rotate_bytes` of activated weights per cycle, at most
+    16 copies), after a short GPU spin that keeps the host ahead.  `shape`
+    overrides the workload's layer shape (same generator); `reject_for(router,
+    shape)` may supply a make_batch rejection callback per sample."""
+    import math
+
     import torch
 
     from . import _lib
     from .pipeline import VerifyPass, pack_expert_weights, to_device, weights_to_device
-    from synth import gen  # the repository root is on sys.path (run from there)
+    from synth import gen
     from synth.configs import WORKLOAD_ID, WORKLOADS
 
     wl = WORKLOADS[workload]
+    shape0 = shape or wl.shape
     wid = WORKLOAD_ID[wl.name]
-    scrub = torch.empty(512 << 20, dtype=torch.uint8, device=device)
     stream = torch.cuda.current_stream()
     samples = []
     for seed in seeds:
-        router = to_device(gen.make_router(wl.shape, seed, 0, wid, wl.router_std), device)
-        experts = gen.make_experts(wl.shape, seed, 0, wid, wl.w_std)
-        shared = gen.make_shared_experts(wl.shape, seed, 0, wid, wl.w_std)
+        experts = gen.make_experts(shape0, seed, 0, wid, wl.w_std)
+        shared = gen.make_shared_experts(shape0, seed, 0, wid, wl.w_std)
         dev_w, _ = weights_to_device(experts, shared, device)
-        packed = wl.shape.wdt != "f32"
+        packed = shape0.wdt != "f32"
         if packed:
-            dev_w, wstruct = pack_expert_weights(dev_w, wl.shape.wdt)
+            dev_w, wstruct = pack_expert_weights(dev_w, shape0.wdt)
         else:
             wstruct = _lib.make_weights(*dev_w)
         del experts, shared
+        copies = [(wstruct, None)]
         for B in batches:
-            x, conf_w, _ = gen.make_batch(wl.shape, B, seed, 0, wid, wl.rho)
-            xd, cd = to_device(x, device), to_device(conf_w, device)
             for alpha in alphas:
-                shape = wl.shape.with_(alpha=alpha)
+                shape = shape0.with_(alpha=alpha)
+                rf = (lambda r, sh=shape: reject_for(r, sh)) if reject_for is not None else None
+                router, x, conf_w = sample_inputs(wl, shape, B, seed, rf)
+                rd, xd, cd = (to_device(a, device) for a in (router, x, conf_w))
                 layer = _lib.make_layer(shape, flags=shape.flags | (
                     _lib.PACKED_WEIGHTS if packed else 0))
                 p = VerifyPass(layer, B, device)
-                p(xd, router, cd, wstruct)
+                p(xd, rd, cd, wstruct)
                 torch.cuda.synchronize()
                 n_uniq = int(p.rt.n_uniq.item())
-                t_step, t_ffn = [], []
-                for i in range(steps):
-                    e = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
-                    scrub.fill_(i & 0xFF)
-                    e[0].record(stream)
-                    p.route(xd, router)
-                    p.reuse_gate(cd)
-                    e[1].record(stream)
-                    p.verify_moe(xd, wstruct)
-                    e[2].record(stream)
-                    p.combine()
-                    e[3].record(stream)
+                nbytes = (n_uniq * expert_bytes(shape, shape.ffn) +
+                          shape.n_shared * expert_bytes(shape, shape.ffn_shared))
+                want = max(1, min(16, math.ceil(rotate_bytes / max(1, nbytes))))
+                while len(copies) < want:
+                    ce = {n: t.clone() for n, t in dev_w[0].items()}
+                    cs = {n: t.clone() for n, t in dev_w[1].items()}
+                    copies.append((_lib.make_weights(ce, cs), (ce, cs)))
+                ws = [c[0] for c in copies[:want]]
+                for w in ws:
+                    p(xd, rd, cd, w)
+                torch.cuda.synchronize()
+                t = {}
+                for kind in ("step", "ffn"):
+                    e0 = torch.cuda.Event(enable_timing=True)
+                    e1 = torch.cuda.Event(enable_timing=True)
+                    torch.cuda._sleep(2_000_000)
+                    e0.record(stream)
+                    for i in range(steps):
+                        if kind == "step":
+                            p(xd, rd, cd, ws[i % want])
+                        else:
+                            p.verify_moe(xd, ws[i % want])
+                    e1.record(stream)
                     torch.cuda.synchronize()
-                    t_step.append(e[0].elapsed_time(e[3]) * 1e3)
-                    t_ffn.append(e[1].elapsed_time(e[2]) * 1e3)
+                    t[kind] = e0.elapsed_time(e1) * 1e3 / steps
                 samples.append({"B": B, "alpha": alpha, "seed": seed, "n_uniq": n_uniq,
-                                "n_shared": shape.n_shared,
-                                "t_step_us": float(np.median(t_step)),
-                                "t_ffn_us": float(np.median(t_ffn))})
+                                "n_shared": shape.n_shared, "weight_copies": want,
+                                "t_step_us": t["step"], "t_ffn_us": t["ffn"]})
                 print(json.dumps(samples[-1]), file=sys.stderr, flush=True)
-        del dev_w, wstruct
+        del dev_w, wstruct, copies
         torch.cuda.empty_cache()
     return samples
 
