@@ -17,7 +17,9 @@
 // the 8-blocks of each super-step stored so that one token's 16 bytes for
 // MFMA j of the four K slots lie side by side.
 //
-// Work decomposition (one persistent launch per projection):
+// Work decomposition for batches of more than kQ4KsplitMaxTokens tokens (one
+// persistent launch per projection; smaller batches run the K-split kernel
+// further down):
 // - A work item is 16 R W rows of one expert (W = 4 waves, R row tiles per
 //   wave) over one of Q contiguous K parts, for all tokens routed to that
 //   expert.  The launch has at most as many workgroups as fit on the GPU at
@@ -173,6 +175,220 @@ __device__ __forceinline__ void compute_step(const CodesQ<R, NM>& st, const u32x
       }
   }
 }
+
+// ---------------------------------------------------------------------------
+// K-split kernel for tiny batches (B <= kQ4KsplitMaxTokens, one token tile):
+// a work unit is R 16-row tiles of one expert over all of K, the W waves of
+// the workgroup split K into contiguous ranges, each loads its own B
+// operands (the batch's few tokens), and the partial tiles are added through
+// LDS in wave order.  Units of 16 R rows (R chosen so the grid still fills
+// the GPU) give a draft step's two or three small experts enough workgroups;
+// the row-split kernel below needs 64- or 128-row items.
+template <int T, int R, int NM>
+struct StageQ {
+  u32x4 c[NM][R];     // one 32-code group per lane
+  uint32_t s[NM][R];  // its fp16 scale (low half)
+  u32x4 b[T][4];      // 4 x 8 activations per token tile
+};
+
+// Codes and scale of super-step s: plain layout -> u32x4 index 4 s and
+// scale index 4 s of the lane's row pointers; packed layout -> 1 KB code
+// tile s and 128-byte scale tile s (nontemporal: read once per call).
+template <bool kPacked, int T, int R, int NM>
+__device__ __forceinline__ void load_q(StageQ<T, R, NM>& st, const u32x4* const* pc,
+                                       const uint16_t* const* ps, const u32x4* const* xb,
+                                       int s) {
+#pragma unroll
+  for (int m = 0; m < NM; ++m)
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      if (kPacked) {
+        st.c[m][r] = __builtin_nontemporal_load(pc[m * R + r] + 64 * s);
+        st.s[m][r] = __builtin_nontemporal_load(ps[m * R + r] + 64 * s);
+      } else {
+        st.c[m][r] = pc[m * R + r][4 * s];
+        st.s[m][r] = ps[m * R + r][4 * s];
+      }
+    }
+#pragma unroll
+  for (int tt = 0; tt < T; ++tt)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) st.b[tt][j] = xb[tt][16 * s + 4 * j];
+}
+
+template <int T, int R, int NM>
+__device__ __forceinline__ void compute_q(const StageQ<T, R, NM>& st, f32x4 (&acc)[NM][R][T],
+                                          uint32_t magic) {
+#pragma unroll
+  for (int m = 0; m < NM; ++m)
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      _Float16 sh;
+      const uint16_t bits = (uint16_t)st.s[m][r];
+      __builtin_memcpy(&sh, &bits, 2);
+      const half2v s2 = {sh, sh};
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const half8v a = q4_decode(st.c[m][r][j], s2, magic);
+#pragma unroll
+        for (int tt = 0; tt < T; ++tt)
+          acc[m][r][tt] = mfma16(a, as_half8(st.b[tt][j]), acc[m][r][tt]);
+      }
+    }
+}
+
+template <int kMode, int T, int TMAX, int R, int W, bool kPacked>
+__device__ __forceinline__ void unit_pass_q(const FfnArgs& a, const Segment& seg, int t0, int r0,
+                                            int K, const uint8_t* C0, const uint8_t* C1,
+                                            const uint16_t* S0, const uint16_t* S1, f32x4* red) {
+  constexpr int NM = kMode == 0 ? 2 : 1;
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wave = wave_id();
+  const int rA = lane & 15, gK = lane >> 4;
+  const int nss = K / 128;
+  const int lo = wave * nss / W, hi = (wave + 1) * nss / W;
+
+  // fp16 activations in decode order: x16 for gate-up, Hh for down.
+  const uint16_t* X = static_cast<const uint16_t*>(kMode == 0 ? a.x16 : a.hh);
+  const int ldx = kMode == 0 ? a.H : a.ldh;
+  const u32x4* xb[T];
+#pragma unroll
+  for (int tt = 0; tt < T; ++tt) {
+    const int t = min(t0 + tt * 16 + rA, seg.n - 1);
+    xb[tt] = reinterpret_cast<const u32x4*>(X + (size_t)x_row(a, kMode, seg, t) * ldx) + gK;
+  }
+  const u32x4* pc[NM * R];
+  const uint16_t* ps[NM * R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    if (kPacked) {
+      const size_t tile0 = (size_t)(r0 / 16 + r) * nss;  // first tile of the row tile
+      pc[r] = reinterpret_cast<const u32x4*>(C0) + tile0 * 64 + lane;
+      ps[r] = S0 + tile0 * 64 + lane;
+      if (NM > 1) {
+        pc[R + r] = reinterpret_cast<const u32x4*>(C1) + tile0 * 64 + lane;
+        ps[R + r] = S1 + tile0 * 64 + lane;
+      }
+    } else {
+      const size_t row = (size_t)(r0 + 16 * r + rA);
+      pc[r] = reinterpret_cast<const u32x4*>(C0 + row * (K / 2)) + gK;
+      ps[r] = S0 + row * (K / 32) + gK;
+      if (NM > 1) {
+        pc[R + r] = reinterpret_cast<const u32x4*>(C1 + row * (K / 2)) + gK;
+        ps[R + r] = S1 + row * (K / 32) + gK;
+      }
+    }
+  }
+
+  f32x4 acc[NM][R][T];
+#pragma unroll
+  for (int m = 0; m < NM; ++m)
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+#pragma unroll
+      for (int tt = 0; tt < T; ++tt) acc[m][r][tt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  if (hi > lo) {
+    const uint32_t magic = opaque(0x64006400u);
+    pipeline2<StageQ<T, R, NM>>(
+        hi - lo,
+        [&](StageQ<T, R, NM>& st, int i) { load_q<kPacked>(st, pc, ps, xb, lo + i); },
+        [&](const StageQ<T, R, NM>& st, int) { compute_q(st, acc, magic); });
+  }
+
+  if (W > 1) {
+    constexpr int kTiles = NM * R * TMAX;
+#pragma unroll
+    for (int m = 0; m < NM; ++m)
+#pragma unroll
+      for (int r = 0; r < R; ++r)
+#pragma unroll
+        for (int tt = 0; tt < T; ++tt)
+          red[(wave * kTiles + (m * R + r) * TMAX + tt) * kWave + lane] = acc[m][r][tt];
+    __syncthreads();
+    if (wave == 0) {
+      for (int w = 1; w < W; ++w) {
+#pragma unroll
+        for (int m = 0; m < NM; ++m)
+#pragma unroll
+          for (int r = 0; r < R; ++r)
+#pragma unroll
+            for (int tt = 0; tt < T; ++tt) {
+              const f32x4 p = red[(w * kTiles + (m * R + r) * TMAX + tt) * kWave + lane];
+#pragma unroll
+              for (int i = 0; i < 4; ++i) acc[m][r][tt][i] += p[i];
+            }
+      }
+    }
+  }
+  if (wave == 0) {
+#pragma unroll
+    for (int tt = 0; tt < T; ++tt) {
+      const int t = t0 + tt * 16 + rA;
+      if (t >= seg.n) continue;
+      if (kMode == 0) {
+        _Float16* dst = static_cast<_Float16*>(a.hh) + (size_t)(seg.base + t) * a.ldh;
+#pragma unroll
+        for (int r = 0; r < R; ++r)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int f = r0 + 16 * r + 4 * gK + i;
+            dst[(block_pos(f >> 3) << 3) | pos8(f & 7)] =
+                (_Float16)(silu(acc[0][r][tt][i]) * acc[NM - 1][r][tt][i]);
+          }
+      } else {
+        float* dst = a.out + (size_t)out_row(a, seg, t) * a.H;
+#pragma unroll
+        for (int r = 0; r < R; ++r)
+          *reinterpret_cast<f32x4*>(dst + r0 + 16 * r + 4 * gK) = acc[0][r][tt];
+      }
+    }
+  }
+  if (W > 1) __syncthreads();
+}
+
+template <int kMode, int TMAX, int R, int W, bool kPacked>
+__global__ __launch_bounds__(W * 64) void ffn_q4_ksplit_kernel(FfnArgs a) {
+  constexpr int NM = kMode == 0 ? 2 : 1;
+  __shared__ f32x4 red[W > 1 ? W * NM * R * TMAX * kWave : 1];
+  Segment seg;
+  int unit;
+  if (!resolve_block(a, kMode, 16 * R, &seg, &unit)) return;
+  const int r0 = unit * 16 * R;
+  const int rows = kMode == 0 ? (seg.shared ? a.Fs : a.F) : a.H;
+  const int K = kMode == 0 ? a.H : (seg.shared ? a.Fs : a.F);
+  const size_t mat = (size_t)rows * K;
+  const void *M0, *M1, *Q0, *Q1;
+  if (kMode == 0) {
+    M0 = seg.shared ? a.sh_gate : a.gate;
+    M1 = seg.shared ? a.sh_up : a.up;
+    Q0 = seg.shared ? a.sh_gate_s : a.gate_s;
+    Q1 = seg.shared ? a.sh_up_s : a.up_s;
+  } else {
+    M0 = M1 = seg.shared ? a.sh_down : a.down;
+    Q0 = Q1 = seg.shared ? a.sh_down_s : a.down_s;
+  }
+  const uint8_t* C0 = static_cast<const uint8_t*>(M0) + seg.id * (mat / 2);
+  const uint8_t* C1 = static_cast<const uint8_t*>(M1) + seg.id * (mat / 2);
+  const uint16_t* S0 = static_cast<const uint16_t*>(Q0) + seg.id * (mat / 32);
+  const uint16_t* S1 = static_cast<const uint16_t*>(Q1) + seg.id * (mat / 32);
+  for (int t0 = 0; t0 < seg.n; t0 += 16 * TMAX) {
+    const int T = min(TMAX, (seg.n - t0 + 15) / 16);
+    if (TMAX >= 4 && T >= 4)
+      unit_pass_q<kMode, (TMAX >= 4 ? 4 : 1), TMAX, R, W, kPacked>(a, seg, t0, r0, K, C0, C1, S0, S1, red);
+    else if (TMAX >= 3 && T == 3)
+      unit_pass_q<kMode, (TMAX >= 3 ? 3 : 1), TMAX, R, W, kPacked>(a, seg, t0, r0, K, C0, C1, S0, S1, red);
+    else if (TMAX >= 2 && T == 2)
+      unit_pass_q<kMode, (TMAX >= 2 ? 2 : 1), TMAX, R, W, kPacked>(a, seg, t0, r0, K, C0, C1, S0, S1, red);
+    else
+      unit_pass_q<kMode, 1, TMAX, R, W, kPacked>(a, seg, t0, r0, K, C0, C1, S0, S1, red);
+  }
+}
+
+// Row-split variant (one or two token tiles per pass): the W waves of a
+// workgroup take different row tiles over all of K, and share the
+// activations, which the workgroup stages in LDS two super-steps at a time
+// (double-buffered, one barrier per two super-steps).  The B operands then
+// come from LDS instead of one global load per wave, which at two token
 
 constexpr int gcd_c(int x, int y) { return y == 0 ? x : gcd_c(y, x % y); }
 constexpr int lcm_c(int x, int y) { return x / gcd_c(x, y) * y; }
@@ -466,6 +682,40 @@ __global__ __launch_bounds__(256) void q4_prep_x_kernel(const uint16_t* __restri
   reinterpret_cast<u32x4*>(x16)[block_pos(i)] = r;
 }
 
+#ifndef S2MOE_Q4_STEPS_PER_WAVE
+#define S2MOE_Q4_STEPS_PER_WAVE 8
+#endif
+
+int pick_waves_q4(int nss, int tiles) {
+  int w = 1;
+  while (w * 2 <= 8 && nss / (w * 2) >= S2MOE_Q4_STEPS_PER_WAVE && (w * 2) * tiles <= 32)
+    w *= 2;
+  return w;
+}
+
+template <int kMode, int TMAX, int R, bool kPacked>
+hipError_t launch_q4_mode_p(const FfnArgs& a, hipStream_t s) {
+  const int nm = kMode == 0 ? 2 : 1;
+  int nss = kMode == 0 ? a.H / 128 : a.F / 128;
+  if (kMode == 1 && a.S > 0) nss = min(nss, a.Fs / 128);
+  const int w = pick_waves_q4(nss, nm * R * TMAX);
+  const dim3 grid(n_blocks(a, kMode, 16 * R));
+  switch (w) {
+    case 1: hipLaunchKernelGGL((ffn_q4_ksplit_kernel<kMode, TMAX, R, 1, kPacked>), grid, dim3(64), 0, s, a); break;
+    case 2: hipLaunchKernelGGL((ffn_q4_ksplit_kernel<kMode, TMAX, R, 2, kPacked>), grid, dim3(128), 0, s, a); break;
+    case 4: hipLaunchKernelGGL((ffn_q4_ksplit_kernel<kMode, TMAX, R, 4, kPacked>), grid, dim3(256), 0, s, a); break;
+    default: hipLaunchKernelGGL((ffn_q4_ksplit_kernel<kMode, TMAX, R, 8, kPacked>), grid, dim3(512), 0, s, a); break;
+  }
+  return hipGetLastError();
+}
+
+template <int kMode, int TMAX, int R>
+hipError_t launch_q4_mode(const FfnArgs& a, hipStream_t s) {
+  return a.packed ? launch_q4_mode_p<kMode, TMAX, R, true>(a, s)
+                  : launch_q4_mode_p<kMode, TMAX, R, false>(a, s);
+}
+
+
 // Compute units of the current device, queried once per device.
 hipError_t device_cus(int* cus) {
   static std::atomic<int> cache[64];
@@ -550,6 +800,19 @@ hipError_t launch_q4_pair(const FfnArgs& a, hipStream_t s) {
   return launch_q4_layout<1, TMAX, S2MOE_Q4_DOWN_R, D, A, C>(a, a.qparts, s);
 }
 
+// Tiny batches: the K-split kernel, with the most row tiles per unit (gate-up
+// 2 or 1, down 4, 2 or 1) that still give every compute unit a workgroup.
+hipError_t launch_q4_ksplit(const FfnArgs& a, hipStream_t s) {
+  int cus = 0;
+  hipError_t err = device_cus(&cus);
+  if (err != hipSuccess) return err;
+  err = n_blocks(a, 0, 32) >= cus ? launch_q4_mode<0, 1, 2>(a, s) : launch_q4_mode<0, 1, 1>(a, s);
+  if (err != hipSuccess) return err;
+  if (n_blocks(a, 1, 64) >= cus) return launch_q4_mode<1, 1, 4>(a, s);
+  if (n_blocks(a, 1, 32) >= cus) return launch_q4_mode<1, 1, 2>(a, s);
+  return launch_q4_mode<1, 1, 1>(a, s);
+}
+
 }  // namespace
 
 hipError_t launch_ffn_q4(const FfnArgs& a, hipStream_t s) {
@@ -558,6 +821,7 @@ hipError_t launch_ffn_q4(const FfnArgs& a, hipStream_t s) {
                      static_cast<const uint16_t*>(a.x), static_cast<uint16_t*>(a.x16), n8);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
+  if (a.B <= kQ4KsplitMaxTokens) return launch_q4_ksplit(a, s);
   // Token tiles held in one pass: the batch bounds every bucket.
   if (a.B <= 16) err = launch_q4_pair<1>(a, s);
   else if (a.B <= 32) err = launch_q4_pair<2>(a, s);

@@ -86,7 +86,12 @@ constexpr int kQ4DownRows = 128;
 #define S2MOE_Q4_DOWN_ITEMS 256
 #endif
 
+// Batches of at most this many tokens run the int4 FFN on the K-split
+// kernel, whose down projection needs no K parts.
+constexpr int kQ4KsplitMaxTokens = 8;
+
 inline int q4_down_parts(int B, int k, int E, int H, int F, int S, int Fs) {
+  if (B <= kQ4KsplitMaxTokens) return 1;
   const int slots = E < B * k ? E : B * k;
   const int items = (S + slots) * (H / kQ4DownRows);
   int q = (S2MOE_Q4_DOWN_ITEMS + items - 1) / items;
