@@ -216,6 +216,54 @@ def test_int4_row_split_gate_up(hidden, B, seed):
     check_outputs(got, ref, "q4g32", label)
 
 
+def _bf16_scaled(bits, factor):
+    """bf16 bit patterns times a power of two (exact away from the ends of
+    the range, which the test's values stay clear of)."""
+    f = (bits.astype(np.uint32) << 16).view(np.float32) * np.float32(factor)
+    u = f.view(np.uint32)
+    assert not (u & 0xFFFF).any()
+    return (u >> 16).astype(np.uint16)
+
+
+@pytest.mark.parametrize("B,seed", [(4, 81), (64, 82)])
+def test_int4_fp16_range_large_magnitudes(B, seed):
+    """int4 weights with values near the top of the fp16 range the header
+    allows: x times 2^12 (|x| up to about 1.6e4) and the router times 2^-12,
+    which leaves every logit, and so the routing, exactly as drawn; gate and
+    up scales times 2^-5, so the SwiGLU activations Hh reach 1.2e4-1.8e4.
+    B = 4 runs the K-split kernel, B = 64 the row-split one with four token
+    tiles; packed equal to row-major bit for bit; outputs against the
+    oracle at the int4 tolerance."""
+    from oracle.s2moe_oracle import silu
+    shape = LayerShape(hidden=256, ffn=512, n_experts=8, top_k=2, cap=4, alpha=0.5, act="bf16",
+                       wdt="q4g32")
+    d = make_inputs(shape, B, seed=seed, rho=0.5)
+    d["x"] = _bf16_scaled(d["x"], 4096.0)
+    d["router"] = _bf16_scaled(d["router"], 1.0 / 4096.0)
+    ex = d["experts"]
+    for n in ("gate_s", "up_s"):
+        s16 = (ex[n].astype(np.float32) / 32).astype(np.float16)
+        assert np.array_equal(s16.astype(np.float32) * 32, ex[n].astype(np.float32))
+        ex[n] = s16
+    W = {n: np.stack([oracle.dequant_q4g32(ex[n][e], ex[n + "_s"][e])
+                      for e in range(shape.n_experts)]) for n in ("gate", "up", "down")}
+    x = oracle.upcast(d["x"], "bf16")
+    hh = silu(np.einsum("bh,efh->ebf", x, W["gate"])) * np.einsum("bh,efh->ebf", x, W["up"])
+    x_max, hh_max = float(np.abs(x).max()), float(np.abs(hh).max())
+    assert x_max >= 1.2e4 and 1e4 <= hh_max < 65504 / 2, (x_max, hh_max)
+    label = f"int4 fp16 range B={B} |x|max={x_max:.0f} |Hh|max={hh_max:.0f}"
+    log(f"[parity] {label}")
+    got, _ = run_gpu(shape, d)
+    packed, _ = run_gpu(shape, d, packed=True)
+    assert np.array_equal(packed["expert_out"], got["expert_out"]), label
+    ref = oracle.forward(d["x"], d["router"], d["conf_w"],
+                         {n: w.astype(np.float32) for n, w in W.items()}, {},
+                         shape.with_(wdt="f32"))
+    check_routing(got, ref, label)
+    errs = check_outputs(got, ref, "q4g32", label)
+    log(f"[parity] {label}: ok errs={errs}")
+
+
 def test_max_hidden():
     """H = 16384 (the documented maximum): long router rows and gate-up
     rows, bf16, small B."""
