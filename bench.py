@@ -353,6 +353,19 @@ def bench_draft(args) -> int:
     torch.cuda.synchronize()
     graph_s = e0.elapsed_time(e1) / 1e3 / args.steps
     achieved = nbytes / graph_s / 1e9
+    # The same step with every layer as four separate calls (route,
+    # reuse_gate, verify_moe, combine), replayed from its own graph.
+    step4 = draft.DraftStep(layer, B, inputs, fused=False)
+    step4.capture()
+    step4.replay()
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(args.steps):
+        step4.replay()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    graph4_s = e0.elapsed_time(e1) / 1e3 / args.steps
+    del step4
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -402,6 +415,7 @@ def bench_draft(args) -> int:
                      "bytes_per_launch": nbytes, "avg_launch_us": graph_s * 1e6},
         "cpu_baseline": cpu,
         "eager_ms_per_step": eager_s * 1e3,
+        "four_call_graph_ms_per_step": graph4_s * 1e3,
         "graph_speedup": eager_s / graph_s,
         "experts_per_step": sum(n_uniq),
     }

@@ -221,6 +221,29 @@ s2moe_status s2moe_combine(const s2moe_layer *layer, int32_t n_tokens,
                            const s2moe_routing *r, const float *expert_out, float *y,
                            void *stream);
 
+/* One whole MoE layer (the verify pass of Sec. "Reuse-aware Expert Gating"
+   over one layer, or a draft step's layer with top_k = k_draft and alpha =
+   0, Sec. "System Implementation", "Draft configuration"): s2moe_route,
+   s2moe_reuse_gate, s2moe_verify_moe and s2moe_combine on these arguments,
+   in that order, with the same results bit for bit in every output (r's
+   arrays, expert_out, y) and the same argument checks and errors.
+   A batch whose gating cannot move the plain top-k (alpha = 0, or
+   n_tokens = 1) and that has at most 4 tokens, BF16 weights and at most 16
+   waves' worth of segments (S + min(E, B k) segments, each taking as many
+   waves as the down launch splits its K into) runs as three launches
+   instead of six: the router rows; the gate-up projection, where every
+   workgroup first ranks the logits and buckets the batch itself; and the
+   down projection with the combine folded in.  Every other batch runs the
+   four calls' kernels one after another.  Layer dispatch cost dominates
+   such small batches (a draft step runs one per MoE layer and token).
+   Workspace, ownership and stream as for s2moe_verify_moe; y as for
+   s2moe_combine. */
+s2moe_status s2moe_moe_layer(const s2moe_layer *layer, int32_t n_tokens, const void *x,
+                             const void *router, const float *conf_w,
+                             const s2moe_weights *w, const s2moe_routing *r,
+                             void *workspace, size_t workspace_bytes, float *expert_out,
+                             float *y, void *stream);
+
 /* ---------------------------------------------------------------------------
    Routing-aware adaptive speculative expansion (Sec. "Routing-aware Adaptive
    Speculative Expansion"): which draft tokens enter the verify batch.

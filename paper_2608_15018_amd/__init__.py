@@ -27,6 +27,7 @@ from ._lib import (  # noqa: F401
     load,
     make_layer,
     make_weights,
+    moe_layer,
     pack_weights,
     reuse_gate,
     route,

@@ -88,6 +88,8 @@ def load():
     lib.s2moe_verify_moe_noalloc.argtypes = [Lp, ctypes.c_int32, P, ctypes.POINTER(Weights),
                                              ctypes.POINTER(RoutingStruct), P, P]
     lib.s2moe_combine.argtypes = [Lp, ctypes.c_int32, ctypes.POINTER(RoutingStruct), P, P, P]
+    lib.s2moe_moe_layer.argtypes = [Lp, ctypes.c_int32, P, P, P, ctypes.POINTER(Weights),
+                                    ctypes.POINTER(RoutingStruct), P, ctypes.c_size_t, P, P, P]
     lib.s2moe_pack_weights.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
                                        ctypes.c_int32, P, P, P, P, P]
     lib.s2moe_pack_weights.restype = ctypes.c_int
@@ -99,7 +101,7 @@ def load():
     lib.s2moe_stream_read.argtypes = [P, ctypes.c_size_t, P, P]
     lib.s2moe_stream_read.restype = ctypes.c_int
     for f in ("s2moe_route", "s2moe_reuse_gate", "s2moe_verify_moe", "s2moe_verify_moe_noalloc",
-              "s2moe_combine"):
+              "s2moe_combine", "s2moe_moe_layer"):
         getattr(lib, f).restype = ctypes.c_int
     lib.s2moe_last_error.restype = ctypes.c_char_p
     lib.s2moe_last_error.argtypes = []
@@ -254,6 +256,16 @@ NOALLOC_SCRATCH_BYTES = 8 << 20
 def combine(layer: Layer, rt: Routing, expert_out: torch.Tensor, y: torch.Tensor, stream=None):
     _check(load().s2moe_combine(ctypes.byref(layer), rt.B, ctypes.byref(rt.struct),
                                 _ptr(expert_out), _ptr(y), _stream(stream)))
+
+
+def moe_layer(layer: Layer, x: torch.Tensor, router: torch.Tensor, conf_w: torch.Tensor,
+              weights: Weights, rt: Routing, workspace: torch.Tensor, expert_out: torch.Tensor,
+              y: torch.Tensor, stream=None):
+    """s2moe_moe_layer: route, reuse_gate, verify_moe and combine in one call."""
+    _check(load().s2moe_moe_layer(ctypes.byref(layer), rt.B, _ptr(x), _ptr(router), _ptr(conf_w),
+                                  ctypes.byref(weights), ctypes.byref(rt.struct), _ptr(workspace),
+                                  workspace.numel() * workspace.element_size(), _ptr(expert_out),
+                                  _ptr(y), _stream(stream)))
 
 
 def pack_weights(wdt: str, mats: torch.Tensor, scales: torch.Tensor | None = None,

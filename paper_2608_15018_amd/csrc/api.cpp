@@ -11,6 +11,8 @@
 #include "kernels.h"
 #include "s2moe.h"
 
+static_assert(s2moe::kMaxShared == S2MOE_MAX_SHARED, "shared-expert limit");
+
 namespace {
 
 thread_local std::string g_last_error;
@@ -140,6 +142,115 @@ s2moe_status hip_status(const char* fn, hipError_t err) {
   return ok();
 }
 
+// Checks of each step's arguments, then its launch struct.  The single
+// entry points and s2moe_moe_layer share them.
+s2moe_status route_args(const char* fn, const s2moe_layer* layer, int32_t n_tokens,
+                        const void* x, const void* router, const s2moe_routing* r,
+                        s2moe::RouteArgs* out) {
+  s2moe_status st = check_layer(fn, layer, n_tokens);
+  if (st != S2MOE_OK) return st;
+  if (r == nullptr) return fail(S2MOE_EINVAL, "%s: routing is NULL", fn);
+  S2MOE_REQUIRE_PTR(x);
+  S2MOE_REQUIRE_PTR(router);
+  S2MOE_REQUIRE_PTR(r->logits);
+  S2MOE_REQUIRE_PTR(r->gap);
+  S2MOE_REQUIRE_PTR(r->plain_idx);
+  s2moe::RouteArgs& a = *out;
+  a.x = x;
+  a.router = router;
+  a.logits = r->logits;
+  a.plain_idx = r->plain_idx;
+  a.gap = r->gap;
+  a.B = n_tokens;
+  a.H = layer->hidden;
+  a.E = layer->n_experts;
+  a.k = layer->top_k;
+  a.bf16 = layer->act_dtype == S2MOE_BF16;
+  return S2MOE_OK;
+}
+
+s2moe_status gate_args(const char* fn, const s2moe_layer* layer, int32_t n_tokens,
+                       const float* conf_w, const s2moe_routing* r, s2moe::GateArgs* out) {
+  s2moe_status st = check_layer(fn, layer, n_tokens);
+  if (st != S2MOE_OK) return st;
+  if (r == nullptr) return fail(S2MOE_EINVAL, "%s: routing is NULL", fn);
+  S2MOE_REQUIRE_PTR(conf_w);
+  S2MOE_REQUIRE_PTR(r->logits);
+  S2MOE_REQUIRE_PTR(r->gap);
+  S2MOE_REQUIRE_PTR(r->plain_idx);
+  S2MOE_REQUIRE_PTR(r->g);
+  S2MOE_REQUIRE_PTR(r->pref);
+  S2MOE_REQUIRE_PTR(r->idx);
+  S2MOE_REQUIRE_PTR(r->gate_w);
+  S2MOE_REQUIRE_PTR(r->count);
+  S2MOE_REQUIRE_PTR(r->offset);
+  S2MOE_REQUIRE_PTR(r->slot);
+  S2MOE_REQUIRE_PTR(r->uniq);
+  S2MOE_REQUIRE_PTR(r->n_uniq);
+  s2moe::GateArgs& a = *out;
+  a.logits = r->logits;
+  a.gap = r->gap;
+  a.plain_idx = r->plain_idx;
+  a.conf_w = conf_w;
+  a.g = r->g;
+  a.pref = r->pref;
+  a.idx = r->idx;
+  a.gate_w = r->gate_w;
+  a.count = r->count;
+  a.offset = r->offset;
+  a.slot = r->slot;
+  a.uniq = r->uniq;
+  a.n_uniq = r->n_uniq;
+  a.B = n_tokens;
+  a.E = layer->n_experts;
+  a.k = layer->top_k;
+  a.cap = layer->cap;
+  a.alpha = layer->alpha;
+  a.flags = layer->flags;
+  return S2MOE_OK;
+}
+
+s2moe_status combine_args(const char* fn, const s2moe_layer* layer, int32_t n_tokens,
+                          const s2moe_routing* r, const float* expert_out, float* y,
+                          s2moe::CombineArgs* out) {
+  s2moe_status st = check_layer(fn, layer, n_tokens);
+  if (st != S2MOE_OK) return st;
+  if (r == nullptr) return fail(S2MOE_EINVAL, "%s: routing is NULL", fn);
+  S2MOE_REQUIRE_PTR(r->gate_w);
+  S2MOE_REQUIRE_PTR(expert_out);
+  S2MOE_REQUIRE_PTR(y);
+  {
+    const size_t H = (size_t)layer->hidden, B = (size_t)n_tokens;
+    const char* e0 = reinterpret_cast<const char*>(expert_out);
+    const char* y0 = reinterpret_cast<const char*>(y);
+    const size_t eb = (B * layer->top_k + (size_t)layer->n_shared * B) * H * sizeof(float);
+    const size_t yb = B * H * sizeof(float);
+    if (y0 < e0 + eb && e0 < y0 + yb)
+      return fail(S2MOE_EINVAL, "%s: y overlaps expert_out", fn);
+  }
+  s2moe::CombineArgs& a = *out;
+  a.gate_w = r->gate_w;
+  a.expert_out = expert_out;
+  a.y = y;
+  a.B = n_tokens;
+  a.H = layer->hidden;
+  a.k = layer->top_k;
+  a.S = layer->n_shared;
+  return S2MOE_OK;
+}
+
+s2moe_status check_workspace(const char* fn, const s2moe_layer* layer, int32_t n_tokens,
+                             const void* workspace, size_t given) {
+  const size_t need = workspace_bytes(layer, n_tokens);
+  if (workspace == nullptr)
+    return fail(S2MOE_EWORKSPACE, "%s: workspace is NULL (%zu bytes needed)", fn, need);
+  if (!aligned16(workspace))
+    return fail(S2MOE_EINVAL, "%s: workspace is not 16-byte aligned", fn);
+  if (given < need)
+    return fail(S2MOE_EWORKSPACE, "%s: workspace holds %zu bytes, %zu needed", fn, given, need);
+  return S2MOE_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -162,67 +273,18 @@ const char* s2moe_status_string(s2moe_status st) {
 s2moe_status s2moe_route(const s2moe_layer* layer, int32_t n_tokens, const void* x,
                          const void* router, const s2moe_routing* r, void* stream) {
   const char* fn = "s2moe_route";
-  s2moe_status st = check_layer(fn, layer, n_tokens);
-  if (st != S2MOE_OK) return st;
-  if (r == nullptr) return fail(S2MOE_EINVAL, "%s: routing is NULL", fn);
-  S2MOE_REQUIRE_PTR(x);
-  S2MOE_REQUIRE_PTR(router);
-  S2MOE_REQUIRE_PTR(r->logits);
-  S2MOE_REQUIRE_PTR(r->gap);
-  S2MOE_REQUIRE_PTR(r->plain_idx);
   s2moe::RouteArgs a;
-  a.x = x;
-  a.router = router;
-  a.logits = r->logits;
-  a.plain_idx = r->plain_idx;
-  a.gap = r->gap;
-  a.B = n_tokens;
-  a.H = layer->hidden;
-  a.E = layer->n_experts;
-  a.k = layer->top_k;
-  a.bf16 = layer->act_dtype == S2MOE_BF16;
+  const s2moe_status st = route_args(fn, layer, n_tokens, x, router, r, &a);
+  if (st != S2MOE_OK) return st;
   return hip_status(fn, s2moe::launch_route(a, static_cast<hipStream_t>(stream)));
 }
 
 s2moe_status s2moe_reuse_gate(const s2moe_layer* layer, int32_t n_tokens, const float* conf_w,
                               const s2moe_routing* r, void* stream) {
   const char* fn = "s2moe_reuse_gate";
-  s2moe_status st = check_layer(fn, layer, n_tokens);
-  if (st != S2MOE_OK) return st;
-  if (r == nullptr) return fail(S2MOE_EINVAL, "%s: routing is NULL", fn);
-  S2MOE_REQUIRE_PTR(conf_w);
-  S2MOE_REQUIRE_PTR(r->logits);
-  S2MOE_REQUIRE_PTR(r->gap);
-  S2MOE_REQUIRE_PTR(r->plain_idx);
-  S2MOE_REQUIRE_PTR(r->g);
-  S2MOE_REQUIRE_PTR(r->pref);
-  S2MOE_REQUIRE_PTR(r->idx);
-  S2MOE_REQUIRE_PTR(r->gate_w);
-  S2MOE_REQUIRE_PTR(r->count);
-  S2MOE_REQUIRE_PTR(r->offset);
-  S2MOE_REQUIRE_PTR(r->slot);
-  S2MOE_REQUIRE_PTR(r->uniq);
-  S2MOE_REQUIRE_PTR(r->n_uniq);
   s2moe::GateArgs a;
-  a.logits = r->logits;
-  a.gap = r->gap;
-  a.plain_idx = r->plain_idx;
-  a.conf_w = conf_w;
-  a.g = r->g;
-  a.pref = r->pref;
-  a.idx = r->idx;
-  a.gate_w = r->gate_w;
-  a.count = r->count;
-  a.offset = r->offset;
-  a.slot = r->slot;
-  a.uniq = r->uniq;
-  a.n_uniq = r->n_uniq;
-  a.B = n_tokens;
-  a.E = layer->n_experts;
-  a.k = layer->top_k;
-  a.cap = layer->cap;
-  a.alpha = layer->alpha;
-  a.flags = layer->flags;
+  const s2moe_status st = gate_args(fn, layer, n_tokens, conf_w, r, &a);
+  if (st != S2MOE_OK) return st;
   return hip_status(fn, s2moe::launch_reuse_gate(a, static_cast<hipStream_t>(stream)));
 }
 
@@ -332,15 +394,8 @@ s2moe_status s2moe_verify_moe(const s2moe_layer* layer, int32_t n_tokens, const 
   const char* fn = "s2moe_verify_moe";
   s2moe::FfnArgs a;
   s2moe_status st = verify_args(fn, layer, n_tokens, x, w, r, expert_out, &a);
+  if (st == S2MOE_OK) st = check_workspace(fn, layer, n_tokens, workspace, workspace_bytes_given);
   if (st != S2MOE_OK) return st;
-  const size_t need = workspace_bytes(layer, n_tokens);
-  if (workspace == nullptr)
-    return fail(S2MOE_EWORKSPACE, "%s: workspace is NULL (%zu bytes needed)", fn, need);
-  if (!aligned16(workspace))
-    return fail(S2MOE_EINVAL, "%s: workspace is not 16-byte aligned", fn);
-  if (workspace_bytes_given < need)
-    return fail(S2MOE_EWORKSPACE, "%s: workspace holds %zu bytes, %zu needed", fn,
-                workspace_bytes_given, need);
   carve_workspace(layer, n_tokens, workspace, &a);
   return hip_status(fn, s2moe::launch_ffn(a, static_cast<hipStream_t>(stream)));
 }
@@ -533,30 +588,37 @@ s2moe_status s2moe_pack_weights(int32_t w_dtype, int32_t n_mats, int32_t rows, i
 s2moe_status s2moe_combine(const s2moe_layer* layer, int32_t n_tokens, const s2moe_routing* r,
                            const float* expert_out, float* y, void* stream) {
   const char* fn = "s2moe_combine";
-  s2moe_status st = check_layer(fn, layer, n_tokens);
-  if (st != S2MOE_OK) return st;
-  if (r == nullptr) return fail(S2MOE_EINVAL, "%s: routing is NULL", fn);
-  S2MOE_REQUIRE_PTR(r->gate_w);
-  S2MOE_REQUIRE_PTR(expert_out);
-  S2MOE_REQUIRE_PTR(y);
-  {
-    const size_t H = (size_t)layer->hidden, B = (size_t)n_tokens;
-    const char* e0 = reinterpret_cast<const char*>(expert_out);
-    const char* y0 = reinterpret_cast<const char*>(y);
-    const size_t eb = (B * layer->top_k + (size_t)layer->n_shared * B) * H * sizeof(float);
-    const size_t yb = B * H * sizeof(float);
-    if (y0 < e0 + eb && e0 < y0 + yb)
-      return fail(S2MOE_EINVAL, "%s: y overlaps expert_out", fn);
-  }
   s2moe::CombineArgs a;
-  a.gate_w = r->gate_w;
-  a.expert_out = expert_out;
-  a.y = y;
-  a.B = n_tokens;
-  a.H = layer->hidden;
-  a.k = layer->top_k;
-  a.S = layer->n_shared;
+  const s2moe_status st = combine_args(fn, layer, n_tokens, r, expert_out, y, &a);
+  if (st != S2MOE_OK) return st;
   return hip_status(fn, s2moe::launch_combine(a, static_cast<hipStream_t>(stream)));
+}
+
+s2moe_status s2moe_moe_layer(const s2moe_layer* layer, int32_t n_tokens, const void* x,
+                             const void* router, const float* conf_w, const s2moe_weights* w,
+                             const s2moe_routing* r, void* workspace,
+                             size_t workspace_bytes_given, float* expert_out, float* y,
+                             void* stream) {
+  const char* fn = "s2moe_moe_layer";
+  s2moe::RouteArgs ra;
+  s2moe::GateArgs ga;
+  s2moe::FfnArgs fa;
+  s2moe::CombineArgs ca;
+  s2moe_status st = route_args(fn, layer, n_tokens, x, router, r, &ra);
+  if (st == S2MOE_OK) st = gate_args(fn, layer, n_tokens, conf_w, r, &ga);
+  if (st == S2MOE_OK) st = verify_args(fn, layer, n_tokens, x, w, r, expert_out, &fa);
+  if (st == S2MOE_OK) st = check_workspace(fn, layer, n_tokens, workspace, workspace_bytes_given);
+  if (st == S2MOE_OK) st = combine_args(fn, layer, n_tokens, r, expert_out, y, &ca);
+  if (st != S2MOE_OK) return st;
+  carve_workspace(layer, n_tokens, workspace, &fa);
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  if (s2moe::moe_layer_small_fits(fa, layer->alpha))
+    return hip_status(fn, s2moe::launch_moe_layer_small(ra, ga, fa, y, s));
+  hipError_t err = s2moe::launch_route(ra, s);
+  if (err == hipSuccess) err = s2moe::launch_reuse_gate(ga, s);
+  if (err == hipSuccess) err = s2moe::launch_ffn(fa, s);
+  if (err == hipSuccess) err = s2moe::launch_combine(ca, s);
+  return hip_status(fn, err);
 }
 
 }  // extern "C"

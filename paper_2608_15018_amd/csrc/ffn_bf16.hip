@@ -13,6 +13,7 @@
 // lane / 16) and 16 bytes of each token tile (B operand, from the
 // L2-resident activations); the R row tiles share the token fragments.
 #include "ffn_common.h"
+#include "small_batch.h"
 
 namespace s2moe {
 
@@ -174,10 +175,11 @@ __device__ __forceinline__ void unit_pass(const FfnArgs& a, const Segment& seg, 
   if (W > 1) __syncthreads();  // LDS is reused by the next pass
 }
 
+// The workgroup's unit: resolve it from the buckets (count, offset, slot,
+// uniq, n_uniq: global, or LDS in the fused small-batch kernel) and run its
+// passes over the tokens.  red: W > 1 ? W NM R TMAX x 64 f32x4 of LDS.
 template <int kMode, int TMAX, int R, int W, int U, bool kPacked>
-__global__ __launch_bounds__(W * 64) void ffn_bf16_kernel(FfnArgs a) {
-  constexpr int NM = kMode == 0 ? 2 : 1;
-  __shared__ f32x4 red[W > 1 ? W * NM * R * TMAX * kWave : 1];
+__device__ __forceinline__ void ffn_bf16_unit(const FfnArgs& a, f32x4* red) {
   Segment seg;
   int unit;
   if (!resolve_block(a, kMode, 16 * R, &seg, &unit)) return;
@@ -204,6 +206,161 @@ __global__ __launch_bounds__(W * 64) void ffn_bf16_kernel(FfnArgs a) {
       unit_pass<kMode, (TMAX >= 2 ? 2 : 1), TMAX, R, W, U, kPacked>(a, seg, t0, r0, K, W0, W1, red);
     else
       unit_pass<kMode, 1, TMAX, R, W, U, kPacked>(a, seg, t0, r0, K, W0, W1, red);
+  }
+}
+
+template <int kMode, int TMAX, int R, int W, int U, bool kPacked>
+__global__ __launch_bounds__(W * 64) void ffn_bf16_kernel(FfnArgs a) {
+  constexpr int NM = kMode == 0 ? 2 : 1;
+  __shared__ f32x4 red[W > 1 ? W * NM * R * TMAX * kWave : 1];
+  ffn_bf16_unit<kMode, TMAX, R, W, U, kPacked>(a, red);
+}
+
+// ------------------------------------------------- fused small-batch layer
+// A whole MoE layer of B <= kSmallMaxTokens tokens whose gating keeps the
+// plain top-k runs as three launches: the router rows (route.hip), then the
+// two kernels below.  Each computes exactly what the unfused kernels
+// compute, so the results are the same bit for bit.
+
+// Gate-up with the routing in its prologue: wave 0 of every workgroup ranks
+// each token's logits and gates the batch (wave_select_plain, small_gate:
+// the code of the routing and gating kernels), leaving the buckets in LDS;
+// workgroup 0 also writes every routing output to global memory.  The unit
+// work is ffn_bf16_kernel<0, ...>'s, resolved from the LDS buckets.
+template <int NJ, int TMAX, int R, int W, int U, bool kPacked>
+__global__ __launch_bounds__(W * 64) void ffn_bf16_gate_up_routed_kernel(FfnArgs a,
+                                                                        RouteArgs ra,
+                                                                        GateArgs ga) {
+  __shared__ SmallGateLds rt;
+  __shared__ f32x4 red[W > 1 ? W * 2 * R * TMAX * kWave : 1];
+  if (wave_id() == 0) {
+    const bool pub = blockIdx.x == 0;
+    for (int b = 0; b < ga.B; ++b)
+      wave_select_plain<NJ>(ra.E, ra.k, ra.logits + (size_t)b * ra.E, rt.plain + b * ra.k,
+                            rt.gap + b, pub ? ra.plain_idx + (size_t)b * ra.k : nullptr,
+                            pub ? ra.gap + b : nullptr);
+    wave_sync();
+    small_gate<NJ>(ga, rt.plain, rt.gap, rt, pub);
+  }
+  __syncthreads();
+  FfnArgs b = a;
+  b.count = rt.count;
+  b.offset = rt.offset;
+  b.slot = rt.slot;
+  b.uniq = rt.uniq;
+  b.n_uniq = &rt.n_uniq;
+  ffn_bf16_unit<0, TMAX, R, W, U, kPacked>(b, red);
+}
+
+// Rows of expert_out a small batch can have: B k + S B.
+constexpr int kSmallOutRows = kSmallMaxTokens * kMaxTopK + kMaxShared * kSmallMaxTokens;
+
+// Down projection and combine in one launch.  A workgroup takes 16 R rows of
+// H for every segment (the shared experts, then the activated experts in
+// uniq order); wave w works on segment w / KW over K part w % KW, the K
+// ranges and the order in which the parts are added being those of the down
+// kernel with KW waves.  The segment's tile goes to expert_out as there and
+// to LDS, and the workgroup then forms y for its rows with the combine
+// kernel's arithmetic (the k routed terms as fmaf in slot order, then the
+// shared terms).
+template <int R, int KW, int U, bool kPacked>
+__global__ __launch_bounds__(1024) void ffn_bf16_down_combine_kernel(FfnArgs a,
+                                                                     const float* gate_w,
+                                                                     float* y) {
+  constexpr int kRows = 16 * R;
+  __shared__ f32x4 red[16 * R * kWave];
+  __shared__ float eo_s[kSmallOutRows][kRows];
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wave = wave_id();
+  const int rA = lane & 15, gK = lane >> 4;
+  const int seg_i = wave / KW, part = wave - seg_i * KW;
+  const int r0 = blockIdx.x * kRows;
+  const int slots = min(a.E, a.B * a.k);
+
+  // Segment of this wave; the same checks as resolve_block.
+  Segment seg;
+  bool live = false;
+  if (seg_i < a.S) {
+    seg.shared = true;
+    seg.id = seg_i;
+    seg.n = a.B;
+    seg.base = a.B * a.k + seg_i * a.B;
+    live = true;
+  } else {
+    const int u = seg_i - a.S;
+    if (u < min(*a.n_uniq, slots)) {
+      const int e = a.uniq[u];
+      if (e >= 0 && e < a.E) {
+        seg.shared = false;
+        seg.id = e;
+        seg.n = a.count[e];
+        seg.base = a.offset[e];
+        live = seg.n > 0 && seg.base >= 0 && seg.base + seg.n <= a.B * a.k;
+      }
+    }
+  }
+
+  f32x4 acc[1][R][1];
+#pragma unroll
+  for (int r = 0; r < R; ++r) acc[0][r][0] = f32x4{0.f, 0.f, 0.f, 0.f};
+  if (live) {
+    const int K = seg.shared ? a.Fs : a.F;
+    const int nks = K / 32;
+    const int lo = part * nks / KW, hi = (part + 1) * nks / KW;
+    const uint16_t* W0 = static_cast<const uint16_t*>(seg.shared ? a.sh_down : a.down) +
+                         (size_t)seg.id * a.H * K;
+    const u32x4* xb[1];
+    xb[0] = reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(a.hh) +
+                                           (size_t)x_row(a, 1, seg, min(rA, seg.n - 1)) *
+                                               a.ldh) +
+            gK;
+    const u32x4* pa[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      if (kPacked)
+        pa[r] = reinterpret_cast<const u32x4*>(W0) + (size_t)(r0 / 16 + r) * nks * 64 + lane;
+      else
+        pa[r] = reinterpret_cast<const u32x4*>(W0 + (size_t)(r0 + 16 * r + rA) * K) + gK;
+    }
+    if (hi > lo) {
+      pipeline2<Stage<1, R, 1, U>>(
+          (hi - lo + U - 1) / U,
+          [&](Stage<1, R, 1, U>& st, int c) { load_stage<kPacked>(st, pa, xb, lo + c * U, hi); },
+          [&](const Stage<1, R, 1, U>& st, int c) { compute_stage(st, acc, lo + c * U, hi); });
+    }
+  }
+  if (KW > 1) {
+#pragma unroll
+    for (int r = 0; r < R; ++r) red[(wave * R + r) * kWave + lane] = acc[0][r][0];
+  }
+  __syncthreads();
+  if (live && part == 0) {
+    for (int w = 1; w < KW; ++w) {
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        const f32x4 p = red[((wave + w) * R + r) * kWave + lane];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) acc[0][r][0][i] += p[i];
+      }
+    }
+    if (rA < seg.n) {
+      const int row = out_row(a, seg, rA);
+      float* dst = a.out + (size_t)row * a.H;
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        *reinterpret_cast<f32x4*>(dst + r0 + 16 * r + 4 * gK) = acc[0][r][0];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) eo_s[row][16 * r + 4 * gK + i] = acc[0][r][0][i];
+      }
+    }
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < a.B * kRows; i += blockDim.x) {
+    const int b = i / kRows, c = i - b * kRows;
+    float v = 0.f;
+    for (int j = 0; j < a.k; ++j) v = fmaf(gate_w[b * a.k + j], eo_s[b * a.k + j][c], v);
+    for (int sh = 0; sh < a.S; ++sh) v += eo_s[a.B * a.k + sh * a.B + b][c];
+    y[(size_t)b * a.H + r0 + c] = v;
   }
 }
 
@@ -246,6 +403,9 @@ hipError_t launch_mode(const FfnArgs& a, int spw, hipStream_t s) {
 // with TMAX so that activation reads from L2 stay below the weight stream.
 // Each choice is (TMAX, R gate-up, steps per stage gate-up, R down, steps
 // per stage down, minimum K steps per wave).
+#ifndef S2MOE_BF16_TINY
+#define S2MOE_BF16_TINY 1, 1, 2, 1, 4, 16
+#endif
 #ifndef S2MOE_BF16_SMALL
 #define S2MOE_BF16_SMALL 1, 1, 2, 1, 4, 16
 #endif
@@ -262,9 +422,81 @@ hipError_t launch_bf16_pair(const FfnArgs& a, hipStream_t s) {
   return err != hipSuccess ? err : launch_mode<1, TMAX, RD, UD>(a, SPW, s);
 }
 
+// The fused small-batch layer with the tiny-batch configuration above: the
+// gate-up and down launches take the waves, rows and stages the unfused
+// launches take, so the arithmetic is the same.
+constexpr int kFusedMaxWaves = 16;
+
+template <int TMAX, int RG, int UG, int RD, int UD, int SPW>
+struct SmallLayer {
+  static_assert(TMAX == 1, "one token tile");
+  static int down_waves(const FfnArgs& a) {
+    int nks = a.F / 32;
+    if (a.S > 0) nks = min(nks, a.Fs / 32);
+    return pick_waves(nks, RD * TMAX, SPW);
+  }
+  static bool fits(const FfnArgs& a) {
+    return (a.S + min(a.E, a.B * a.k)) * down_waves(a) <= kFusedMaxWaves;
+  }
+
+  template <int NJ, bool kPacked>
+  static hipError_t gate_up(const FfnArgs& a, const RouteArgs& ra, const GateArgs& ga,
+                            hipStream_t s) {
+    const int w = pick_waves(a.H / 32, 2 * RG * TMAX, SPW);
+    const dim3 grid(n_blocks(a, 0, 16 * RG));
+    switch (w) {
+      case 1: hipLaunchKernelGGL((ffn_bf16_gate_up_routed_kernel<NJ, TMAX, RG, 1, UG, kPacked>), grid, dim3(64), 0, s, a, ra, ga); break;
+      case 2: hipLaunchKernelGGL((ffn_bf16_gate_up_routed_kernel<NJ, TMAX, RG, 2, UG, kPacked>), grid, dim3(128), 0, s, a, ra, ga); break;
+      case 4: hipLaunchKernelGGL((ffn_bf16_gate_up_routed_kernel<NJ, TMAX, RG, 4, UG, kPacked>), grid, dim3(256), 0, s, a, ra, ga); break;
+      default: hipLaunchKernelGGL((ffn_bf16_gate_up_routed_kernel<NJ, TMAX, RG, 8, UG, kPacked>), grid, dim3(512), 0, s, a, ra, ga); break;
+    }
+    return hipGetLastError();
+  }
+
+  template <bool kPacked>
+  static hipError_t down(const FfnArgs& a, const float* gate_w, float* y, hipStream_t s) {
+    const int kw = down_waves(a);
+    const dim3 grid(a.H / (16 * RD));
+    const dim3 block(64 * kw * (a.S + min(a.E, a.B * a.k)));
+    switch (kw) {
+      case 1: hipLaunchKernelGGL((ffn_bf16_down_combine_kernel<RD, 1, UD, kPacked>), grid, block, 0, s, a, gate_w, y); break;
+      case 2: hipLaunchKernelGGL((ffn_bf16_down_combine_kernel<RD, 2, UD, kPacked>), grid, block, 0, s, a, gate_w, y); break;
+      case 4: hipLaunchKernelGGL((ffn_bf16_down_combine_kernel<RD, 4, UD, kPacked>), grid, block, 0, s, a, gate_w, y); break;
+      default: hipLaunchKernelGGL((ffn_bf16_down_combine_kernel<RD, 8, UD, kPacked>), grid, block, 0, s, a, gate_w, y); break;
+    }
+    return hipGetLastError();
+  }
+
+  template <bool kPacked>
+  static hipError_t layer(const RouteArgs& ra, const GateArgs& ga, const FfnArgs& a, float* y,
+                          hipStream_t s) {
+    hipError_t err = launch_route_rows(ra, s);
+    if (err != hipSuccess) return err;
+    if (a.E <= 64) err = gate_up<1, kPacked>(a, ra, ga, s);
+    else if (a.E <= 128) err = gate_up<2, kPacked>(a, ra, ga, s);
+    else err = gate_up<4, kPacked>(a, ra, ga, s);
+    if (err != hipSuccess) return err;
+    return down<kPacked>(a, ga.gate_w, y, s);
+  }
+};
+
+using TinyLayer = SmallLayer<S2MOE_BF16_TINY>;
+
 }  // namespace
 
+bool moe_layer_small_fits(const FfnArgs& a, float alpha) {
+  return a.wf == kWBf16 && a.B >= 1 && a.B <= kSmallMaxTokens && (alpha == 0.f || a.B == 1) &&
+         TinyLayer::fits(a);
+}
+
+hipError_t launch_moe_layer_small(const RouteArgs& ra, const GateArgs& ga, const FfnArgs& a,
+                                  float* y, hipStream_t s) {
+  return a.packed ? TinyLayer::layer<true>(ra, ga, a, y, s)
+                  : TinyLayer::layer<false>(ra, ga, a, y, s);
+}
+
 hipError_t launch_ffn_bf16(const FfnArgs& a, hipStream_t s) {
+  if (a.B <= 4) return launch_bf16_pair<S2MOE_BF16_TINY>(a, s);
   if (a.B <= 16) return launch_bf16_pair<S2MOE_BF16_SMALL>(a, s);
   if (a.B <= 32) return launch_bf16_pair<S2MOE_BF16_MEDIUM>(a, s);
   return launch_bf16_pair<S2MOE_BF16_LARGE>(a, s);

@@ -17,13 +17,11 @@
 //     below its token.
 // Every result is deterministic: integer atomics only (bitwise OR), fixed
 // floating-point summation orders, rank-based placement.
-#include "kernels.h"
-#include "select.h"
+#include "small_batch.h"
 
 namespace s2moe {
 
 constexpr int kStage = 10240;  // logits staged in LDS up to B * E = 10240
-constexpr float kLog2e = 1.4426950408889634f;
 
 // kNJ = expert slots per lane (E <= 64 kNJ); kNT = tokens a wave takes
 // through the threshold search together.
@@ -260,182 +258,15 @@ __global__ __launch_bounds__(1024) void reuse_gate_kernel(GateArgs a) {
   }
 }
 
-// Small batches without a bias that can change the selection: alpha = 0
-// (then ell' = ell), or a single token (its top-k lies inside E* = TopCap(w
-// ell) whatever the flags, and every member of E* gets the same lambda, so
-// the biased top-k is the plain one).  One wave computes g and E* as the
-// kernel above does (same runs of tokens, same ranking order), copies the
-// plain top-k, forms the gate weights with the same arithmetic and buckets
-// the B k <= 64 assignments, with no workgroup barriers between the phases.
-constexpr int kSmallMaxTokens = 4;
-
+// Small batches without a bias that can change the selection (alpha = 0,
+// or a single token): one wave (small_gate) computes g and E* as the kernel
+// above does, takes the plain top-k, forms the gate weights with the same
+// arithmetic and buckets the B k <= 64 assignments, with no workgroup
+// barriers between the phases.
 template <int kNJ>
 __global__ __launch_bounds__(kWave) void reuse_gate_small_kernel(GateArgs a) {
-  __shared__ int count_s[kMaxExperts];
-  __shared__ int offset_s[kMaxExperts];
-  __shared__ int cand_s[kMaxExperts];
-  __shared__ int idx_s[kWave];
-  const int lane = threadIdx.x;
-  const int B = a.B, E = a.E, k = a.k, n_asg = B * k;
-
-  // Every global read is issued up front: confidences, gaps, the plain top-k
-  // and all B x E logits (at most 4 x 4 per lane).
-  float w[kSmallMaxTokens], gap[kSmallMaxTokens], lg[kSmallMaxTokens][kNJ];
-  int active = 0;
-#pragma unroll
-  for (int b = 0; b < kSmallMaxTokens; ++b) {
-    w[b] = b < B ? fmaxf(a.conf_w[b], 0.f) : 0.f;
-    gap[b] = b < B ? a.gap[b] : 0.f;
-#pragma unroll
-    for (int j = 0; j < kNJ; ++j) {
-      const int e = lane + kWave * j;
-      lg[b][j] = b < B && e < E ? a.logits[(size_t)b * E + e] : 0.f;
-    }
-    active |= w[b] > 0.f;
-  }
-  const int pidx = lane < n_asg ? a.plain_idx[lane] : 0;
-  const bool activated_only = (a.flags & kPrefActivatedOnly) != 0;
-#pragma unroll
-  for (int j = 0; j < kMaxExperts / kWave; ++j) {
-    const int e = lane + kWave * j;
-    count_s[e] = 0;
-    cand_s[e] = !activated_only && e < E;
-  }
-  // Ids outside [0, E) (plain_idx never computed) are clamped, so that
-  // nothing is addressed out of range.
-  int my_e = 0;
-  if (lane < n_asg) {
-    my_e = min(max(pidx, 0), E - 1);
-    idx_s[lane] = my_e;
-  }
-  __syncthreads();
-  if (lane < n_asg) {
-    if (activated_only) cand_s[my_e] = 1;
-    atomicAdd(&count_s[my_e], 1);
-  }
-  __syncthreads();
-
-  // g_e in the same runs of tokens as the kernel above.
-  int parts = 1;
-  while (parts * 2 * E <= 1024 && parts * 2 <= B) parts *= 2;
-  const int run = (B + parts - 1) / parts;
-  uint32_t key[1][kNJ];
-  int n_cand = 0;
-#pragma unroll
-  for (int j = 0; j < kNJ; ++j) {
-    const int e = lane + kWave * j;
-    key[0][j] = 0;
-    if (e < E) {
-      float tot = 0.f;
-      for (int part = 0; part < parts; ++part) {
-        float sum = 0.f;
-#pragma unroll
-        for (int b = 0; b < kSmallMaxTokens; ++b)
-          if (b >= part * run && b < min(B, part * run + run)) sum = fmaf(w[b], lg[b][j], sum);
-        tot = part == 0 ? sum : tot + sum;
-      }
-      a.g[e] = tot;
-      if (cand_s[e]) key[0][j] = order_key(tot);
-    }
-    n_cand += __popcll(__ballot(e < E && cand_s[e]));
-  }
-  // E* = the cap candidates of largest g (ties: lower id).
-  uint32_t pref_bits = 0;
-  if (active) {
-    if (n_cand <= a.cap) {
-#pragma unroll
-      for (int j = 0; j < kNJ; ++j)
-        if (key[0][j] != 0) pref_bits |= 1u << j;
-    } else {
-      uint32_t sel[1];
-      wave_top_k<1, kNJ>(key, a.cap, sel);
-      pref_bits = sel[0];
-    }
-  }
-#pragma unroll
-  for (int j = 0; j < kNJ; ++j) {
-    const int e = lane + kWave * j;
-    if (e < E) a.pref[e] = (pref_bits >> j) & 1u;
-  }
-
-  // Per token: the plain top-k and its gate weights.
-  const bool from_biased = (a.flags & kGateFromBiased) != 0;
-#pragma unroll
-  for (int b = 0; b < kSmallMaxTokens; ++b) {
-    if (b >= B) break;
-    const float lam = active ? ((a.flags & kBiasAbsolute) ? a.alpha : a.alpha * gap[b]) : 0.f;
-    uint32_t bits = 0;
-    float x[kNJ];
-#pragma unroll
-    for (int j = 0; j < kNJ; ++j)
-      x[j] = from_biased && ((pref_bits >> j) & 1u) ? lg[b][j] + lam : lg[b][j];
-    for (int q = 0; q < k; ++q) {
-      const int e = idx_s[b * k + q];
-      if ((e & (kWave - 1)) == lane) bits |= 1u << (e / kWave);
-    }
-    uint32_t mk = 0;
-#pragma unroll
-    for (int j = 0; j < kNJ; ++j)
-      if ((bits >> j) & 1u) mk = max(mk, order_key(x[j]));
-    const float m = key_value(wave_max_key_dpp(mk));
-    float ez[kNJ], sum = 0.f;
-#pragma unroll
-    for (int j = 0; j < kNJ; ++j) {
-      ez[j] = ((bits >> j) & 1u) ? __builtin_amdgcn_exp2f((x[j] - m) * kLog2e) : 0.f;
-      sum += ez[j];
-    }
-    const float inv_s = __builtin_amdgcn_rcpf(wave_sum_dpp(sum));
-    int rank[kNJ];
-    wave_rank_flagged<kNJ>(bits, rank);
-#pragma unroll
-    for (int j = 0; j < kNJ; ++j)
-      if ((bits >> j) & 1u) {
-        const int pos = b * k + rank[j];
-        a.idx[pos] = lane + kWave * j;
-        a.gate_w[pos] = ez[j] * inv_s;
-      }
-  }
-
-  // Buckets: counts, exclusive offsets, the activated-expert list, slots.
-  {
-    int c[4], f[4], sum_c = 0, sum_f = 0;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int e = lane * 4 + j;
-      c[j] = e < E ? count_s[e] : 0;
-      f[j] = c[j] > 0;
-      sum_c += c[j];
-      sum_f += f[j];
-    }
-    const int incl_c = wave_inclusive_scan_dpp(sum_c);
-    const int incl_f = wave_inclusive_scan_dpp(sum_f);
-    const int total_c = __builtin_amdgcn_readlane(incl_c, 63);
-    const int total_f = __builtin_amdgcn_readlane(incl_f, 63);
-    int run_c = incl_c - sum_c, run_f = incl_f - sum_f;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int e = lane * 4 + j;
-      if (e < E) {
-        offset_s[e] = run_c;
-        a.offset[e] = run_c;
-        a.count[e] = c[j];
-        if (f[j]) a.uniq[run_f] = e;
-      }
-      run_c += c[j];
-      run_f += f[j];
-    }
-    for (int i = total_f + lane; i < E; i += kWave) a.uniq[i] = -1;
-    if (lane == 0) {
-      a.offset[E] = total_c;
-      *a.n_uniq = total_f;
-    }
-  }
-  __syncthreads();
-  if (lane < n_asg) {
-    int before = 0;
-    for (int q = 0; q < lane; ++q) before += idx_s[q] == my_e;
-    a.slot[offset_s[my_e] + before] = lane;
-  }
+  __shared__ SmallGateLds s;
+  small_gate<kNJ>(a, a.plain_idx, a.gap, s, true);
 }
 
 template <bool kStaged, int kNJ>

@@ -9,6 +9,7 @@ namespace s2moe {
 constexpr int kMaxTopK = 16;
 constexpr int kMaxTokens = 256;
 constexpr int kMaxExperts = 256;
+constexpr int kMaxShared = 8;  // S2MOE_MAX_SHARED
 
 enum : uint32_t {
   kPrefActivatedOnly = 1u,
@@ -174,6 +175,8 @@ hipError_t noalloc_scratch(void** ptr);
 
 hipError_t launch_expand(const ExpandArgs& a, size_t lds_bytes, hipStream_t s);
 hipError_t launch_route(const RouteArgs& a, hipStream_t s);
+// Logits only (the first launch of launch_route's small-batch path).
+hipError_t launch_route_rows(const RouteArgs& a, hipStream_t s);
 hipError_t launch_stream_read(const void* src, size_t bytes, uint32_t* sink, int blocks,
                               hipStream_t s);
 hipError_t launch_pack(const PackArgs& a, hipStream_t s);
@@ -182,5 +185,15 @@ hipError_t launch_ffn(const FfnArgs& a, hipStream_t s);
 hipError_t launch_ffn_bf16(const FfnArgs& a, hipStream_t s);
 hipError_t launch_ffn_q4(const FfnArgs& a, hipStream_t s);
 hipError_t launch_combine(const CombineArgs& a, hipStream_t s);
+
+// A whole MoE layer of a small batch in three launches (router rows, gate-up
+// with the routing in its prologue, down with the combine; ffn_bf16.hip),
+// the same results bit for bit as launch_route, launch_reuse_gate,
+// launch_ffn and launch_combine in sequence.  moe_layer_small_fits tells
+// whether the layer and batch qualify (bf16 weights, B <= 4 with alpha = 0
+// or B = 1, few enough segments); a carries the same buckets as ga.
+bool moe_layer_small_fits(const FfnArgs& a, float alpha);
+hipError_t launch_moe_layer_small(const RouteArgs& ra, const GateArgs& ga, const FfnArgs& a,
+                                  float* y, hipStream_t s);
 
 }  // namespace s2moe

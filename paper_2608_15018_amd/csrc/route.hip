@@ -11,8 +11,7 @@
 // reductions add the lane partials and the slices are summed in order.
 // Wave 0 then ranks the E logits: an exact top-(k+1) by ballots over the
 // order keys, as in the gating kernel.
-#include "kernels.h"
-#include "select.h"
+#include "small_batch.h"
 
 namespace s2moe {
 
@@ -90,52 +89,13 @@ __global__ __launch_bounds__(256) void route_rows_kernel(RouteArgs a) {
   if (lane == 0) a.logits[(size_t)b * a.E + e] = acc;
 }
 
-// Plain top-k and gap of token b by one wave, from its E logits ell (LDS or
-// global): the exact top-(k+1) by (value desc, id asc); its last member
-// (smallest value, then largest id) is the (k+1)-th, the other k are the
-// plain top-k, listed in id order; gap = ell_(1) - ell_(k+1).
-template <int NJ>
-__device__ __forceinline__ void wave_select_plain(const RouteArgs& a, int b, const float* ell) {
-  const int lane = threadIdx.x & (kWave - 1), E = a.E, k = a.k;
-  uint32_t key[1][NJ];
-#pragma unroll
-  for (int j = 0; j < NJ; ++j) {
-    const int e = lane + kWave * j;
-    key[0][j] = e < E ? order_key(ell[e]) : 0u;
-  }
-  uint32_t sel[1];
-  wave_top_k<1, NJ>(key, k + 1, sel);
-  uint32_t mn = 0xFFFFFFFFu, mx = 0u;
-#pragma unroll
-  for (int j = 0; j < NJ; ++j) {
-    if ((sel[0] >> j) & 1u) mn = min(mn, key[0][j]);
-    mx = max(mx, key[0][j]);
-  }
-  mn = ~wave_max_key_dpp(~mn);
-  mx = wave_max_key_dpp(mx);
-  int last = -1;
-#pragma unroll
-  for (int j = NJ - 1; j >= 0; --j) {
-    const uint64_t m = __ballot(((sel[0] >> j) & 1u) && key[0][j] == mn);
-    if (last < 0 && m) last = kWave * j + 63 - __builtin_clzll(m);
-  }
-  uint32_t bits = 0;
-#pragma unroll
-  for (int j = 0; j < NJ; ++j)
-    if (((sel[0] >> j) & 1u) && lane + kWave * j != last) bits |= 1u << j;
-  int rank[NJ];
-  wave_rank_flagged<NJ>(bits, rank);
-#pragma unroll
-  for (int j = 0; j < NJ; ++j)
-    if ((bits >> j) & 1u) a.plain_idx[(size_t)b * k + rank[j]] = lane + kWave * j;
-  if (lane == 0) a.gap[b] = key_value(mx) - key_value(mn);
-}
-
 // Small batches, second launch: one wave per token ranks the logits
 // route_rows_kernel wrote.
 template <int NJ>
 __global__ __launch_bounds__(kWave) void route_select_wave_kernel(RouteArgs a) {
-  wave_select_plain<NJ>(a, blockIdx.x, a.logits + (size_t)blockIdx.x * a.E);
+  const int b = blockIdx.x;
+  wave_select_plain<NJ>(a.E, a.k, a.logits + (size_t)b * a.E, a.plain_idx + (size_t)b * a.k,
+                        a.gap + b, nullptr, nullptr);
 }
 
 template <bool kBf16, int NJ>
@@ -175,7 +135,9 @@ __global__ __launch_bounds__(1024) void route_kernel(RouteArgs a) {
     a.logits[(size_t)b * E + tid] = v;
   }
   __syncthreads();
-  if (wave == 0) wave_select_plain<NJ>(a, b, ell_s);
+  if (wave == 0)
+    wave_select_plain<NJ>(E, a.k, ell_s, a.plain_idx + (size_t)b * a.k, a.gap + b, nullptr,
+                          nullptr);
 }
 
 }  // namespace
@@ -192,14 +154,18 @@ __global__ __launch_bounds__(1024) void route_kernel(RouteArgs a) {
 #define S2MOE_ROUTE_ROWS_MIN_E 64
 #endif
 
+hipError_t launch_route_rows(const RouteArgs& a, hipStream_t s) {
+  const dim3 grid((a.E + 3) / 4, a.B);
+  if (a.bf16)
+    hipLaunchKernelGGL(route_rows_kernel<true>, grid, dim3(256), 0, s, a);
+  else
+    hipLaunchKernelGGL(route_rows_kernel<false>, grid, dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
 hipError_t launch_route(const RouteArgs& a, hipStream_t s) {
   if (a.B <= S2MOE_ROUTE_ROWS_MAX_B || a.E > S2MOE_ROUTE_ROWS_MIN_E) {
-    const dim3 grid((a.E + 3) / 4, a.B);
-    if (a.bf16)
-      hipLaunchKernelGGL(route_rows_kernel<true>, grid, dim3(256), 0, s, a);
-    else
-      hipLaunchKernelGGL(route_rows_kernel<false>, grid, dim3(256), 0, s, a);
-    const hipError_t e = hipGetLastError();
+    const hipError_t e = launch_route_rows(a, s);
     if (e != hipSuccess) return e;
     if (a.E <= 64)
       hipLaunchKernelGGL(route_select_wave_kernel<1>, dim3(a.B), dim3(kWave), 0, s, a);

@@ -11,8 +11,10 @@ verification.  Attention and the rest of the transformer are out of scope:
 each layer takes its own hidden states.
 
 At these shapes a layer streams a few MB of weights, so launch latency
-matters; a `DraftStep` can be captured once in a HIP graph (through torch's
-graph capture of the stream the library calls enqueue on) and replayed.
+matters: each layer is one s2moe_moe_layer call (three launches instead of
+six where the batch allows, the same results bit for bit), and a
+`DraftStep` can be captured once in a HIP graph (through torch's graph
+capture of the stream the library calls enqueue on) and replayed.
 """
 
 from __future__ import annotations
@@ -48,13 +50,16 @@ class DraftStep:
     """One draft step over a stack of layers: for layer l, route ->
     gate -> experts -> combine on inputs (x_l, router_l, weights_l)."""
 
-    def __init__(self, layer: _lib.Layer, B: int, inputs: list, device="cuda"):
-        """inputs: per layer (x [B, H] bf16, router [E, H] bf16, Weights)."""
+    def __init__(self, layer: _lib.Layer, B: int, inputs: list, device="cuda",
+                 fused: bool = True):
+        """inputs: per layer (x [B, H] bf16, router [E, H] bf16, Weights).
+        fused=False runs each layer as the four separate calls instead of one
+        s2moe_moe_layer."""
         self.layer = layer
         self.B = B
         self.inputs = inputs
         self.conf = torch.ones(B, dtype=torch.float32, device=device)
-        self.passes = [VerifyPass(layer, B, device) for _ in inputs]
+        self.passes = [VerifyPass(layer, B, device, fused=fused) for _ in inputs]
         self.graph = None
 
     def __call__(self, stream=None):

@@ -45,11 +45,14 @@ def pack_expert_weights(dev: tuple, wdt: str):
 
 
 class VerifyPass:
-    """Buffers and calls of one verify-MoE layer pass for B draft tokens."""
+    """Buffers and calls of one verify-MoE layer pass for B draft tokens.
+    With fused=True a call is one s2moe_moe_layer (same results bit for bit,
+    fewer launches for small batches); otherwise the four calls in turn."""
 
-    def __init__(self, layer: _lib.Layer, B: int, device="cuda"):
+    def __init__(self, layer: _lib.Layer, B: int, device="cuda", fused: bool = False):
         self.layer = layer
         self.B = B
+        self.fused = fused
         self.rt = _lib.Routing(layer, B, device)
         nbytes = _lib.workspace_bytes(layer, B)
         self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=device)
@@ -70,6 +73,10 @@ class VerifyPass:
         _lib.combine(self.layer, self.rt, self.expert_out, self.y, stream)
 
     def __call__(self, x, router, conf_w, weights: _lib.Weights, stream=None):
+        if self.fused:
+            _lib.moe_layer(self.layer, x, router, conf_w, weights, self.rt, self.workspace,
+                           self.expert_out, self.y, stream)
+            return self.y
         self.route(x, router, stream)
         self.reuse_gate(conf_w, stream)
         self.verify_moe(x, weights, stream)

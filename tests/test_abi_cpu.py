@@ -246,3 +246,52 @@ def test_noalloc_scratch_size_matches_header():
     text = open(_lib.HEADER_PATH).read()
     m = re.search(r"#define S2MOE_NOALLOC_SCRATCH_BYTES \((\d+)u << (\d+)\)", text)
     assert m and int(m.group(1)) << int(m.group(2)) == s2.NOALLOC_SCRATCH_BYTES
+
+
+def test_moe_layer_validates_like_the_four_calls(lib):
+    """s2moe_moe_layer runs the checks of route, reuse_gate, verify_moe (with
+    its workspace) and combine before anything is enqueued."""
+    L = _layer(n_shared=1, ffn_shared=512)
+    B, H = 4, 256
+    w = _lib.Weights(*([0x300000] * 12))
+    rt = _lib.RoutingStruct(*([0x200000] * 12))
+    fake = ctypes.c_void_p(0x100000)
+    need = s2.workspace_bytes(L, B)
+    ws = ctypes.c_void_p(0x400000)
+    eo, y = 0x1000000, 0x2000000
+
+    def call(layer=L, n=B, x=fake, router=fake, conf=fake, weights=w, routing=rt, work=ws,
+             nbytes=need, out=eo, yy=y):
+        st = lib.s2moe_moe_layer(ctypes.byref(layer) if layer is not None else None, n, x, router,
+                                 conf, ctypes.byref(weights), ctypes.byref(routing), work, nbytes,
+                                 ctypes.c_void_p(out) if out else None,
+                                 ctypes.c_void_p(yy) if yy else None, None)
+        return st, _lib.last_error()
+
+    st, msg = call(layer=None)
+    assert st == _lib.EINVAL and "layer" in msg and msg.startswith("s2moe_moe_layer")
+    assert call(n=0)[0] == _lib.EINVAL
+    st, msg = call(router=None)
+    assert st == _lib.EINVAL and "router" in msg
+    st, msg = call(conf=None)
+    assert st == _lib.EINVAL and "conf_w" in msg
+    st, msg = call(work=None)
+    assert st == _lib.EWORKSPACE and "workspace" in msg
+    st, msg = call(nbytes=need - 1)
+    assert st == _lib.EWORKSPACE and str(need) in msg
+    st, msg = call(out=None)
+    assert st == _lib.EINVAL and "expert_out" in msg
+    st, msg = call(yy=None)
+    assert st == _lib.EINVAL and "y" in msg
+    st, msg = call(yy=eo + 16)
+    assert st == _lib.EINVAL and "overlaps" in msg
+    w2 = _lib.Weights(*([0x300000] * 12))
+    w2.sh_up = None
+    st, msg = call(weights=w2)
+    assert st == _lib.EINVAL and "sh_up" in msg
+    rt2 = _lib.RoutingStruct(*([0x200000] * 12))
+    rt2.gate_w = None
+    st, msg = call(routing=rt2)
+    assert st == _lib.EINVAL and "gate_w" in msg
+    st, msg = call(layer=_layer(cap=1))
+    assert st == _lib.EINVAL and "cap" in msg

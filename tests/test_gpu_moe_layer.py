@@ -1,0 +1,174 @@
+"""GPU checks of s2moe_moe_layer, one MoE layer in one call.
+
+* Bit for bit equal to s2moe_route, s2moe_reuse_gate, s2moe_verify_moe and
+  s2moe_combine called in turn, in every routing array, expert_out and y:
+  on batches that take the three-launch path (B <= 4 with alpha = 0, or one
+  token; bf16 weights; E of 8 to 200, so one, two or four experts per lane
+  in the ranking; shared experts; down K split over 1 and 4 waves; packed
+  and row-major weights) and on batches that do not (alpha > 0 at B = 2,
+  too many segments, B = 8, int4 and fp32 weights).
+* The number of launches, read from a captured HIP graph: 3 on the fused
+  path, 6 for the same layer as four calls.
+* Against the oracle on the fused cases (routing exact, outputs within the
+  bf16 tolerance), and graph replays equal to the eager call.
+"""
+
+import ctypes
+
+import numpy as np
+import pytest
+
+import oracle
+from synth.configs import LayerShape
+from tests.gpu_helpers import check_outputs, check_routing, log, make_inputs
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2608_15018_amd as s2
+    s2.load()
+
+
+def _shape(**kw):
+    base = dict(hidden=256, ffn=512, n_experts=8, top_k=2, cap=2, alpha=0.0, act="bf16",
+                wdt="bf16")
+    base.update(kw)
+    return LayerShape(**base)
+
+
+# (label, shape, B, takes the three-launch path)
+CASES = [
+    ("e8 k2 B1", _shape(), 1, True),
+    ("e8 k2 B4", _shape(), 4, True),
+    ("e64 k3 B3 shared", _shape(hidden=512, ffn=256, n_experts=64, top_k=3, cap=3, n_shared=2,
+                                ffn_shared=256), 3, True),
+    ("e128 k3 B1", _shape(hidden=512, n_experts=128, top_k=3, cap=3), 1, True),
+    ("e200 k4 B2", _shape(ffn=384, n_experts=200, top_k=4, cap=4), 2, True),
+    ("F2048 KW4 B1", _shape(ffn=2048, n_experts=16, top_k=3, cap=3), 1, True),
+    ("alpha B1", _shape(n_experts=32, top_k=4, cap=8, alpha=0.7), 1, True),
+    ("alpha flags B1", _shape(n_experts=32, top_k=4, cap=8, alpha=0.5, flags=1 | 4), 1, True),
+    ("alpha B2 (four calls)", _shape(n_experts=32, top_k=4, cap=8, alpha=0.7), 2, False),
+    ("k16 B4 (four calls)", _shape(n_experts=64, top_k=16, cap=16), 4, False),
+    ("F2048 B2 (four calls)", _shape(ffn=2048, n_experts=16, top_k=3, cap=3), 2, False),
+    ("B8 (four calls)", _shape(), 8, False),
+    ("int4 B2 (four calls)", _shape(wdt="q4g32"), 2, False),
+    ("fp32 B1 (four calls)", _shape(act="f32", wdt="f32"), 1, False),
+]
+
+
+def _poison(p):
+    for t in list(vars(p.rt).values()) + [p.expert_out, p.y]:
+        if isinstance(t, torch.Tensor):
+            t.fill_(float("nan") if t.is_floating_point() else -7)
+
+
+def _run(shape, d, fused, packed):
+    import paper_2608_15018_amd as s2
+    from paper_2608_15018_amd.pipeline import pack_expert_weights, to_device, weights_to_device
+    B = d["x"].shape[0]
+    layer = s2.make_layer(shape, flags=shape.flags | (s2.PACKED_WEIGHTS if packed else 0))
+    dev, w = weights_to_device(d["experts"], d["shared"])
+    if packed:
+        dev, w = pack_expert_weights(dev, shape.wdt)
+    p = s2.VerifyPass(layer, B, fused=fused)
+    _poison(p)
+    ins = (to_device(d["x"]), to_device(d["router"]), to_device(d["conf_w"]))
+    torch.cuda.synchronize()
+    p(*ins, w)
+    torch.cuda.synchronize()
+    return p, ins, w, dev
+
+
+def _assert_same(a: dict, b: dict, label):
+    for n in a:
+        x, y = np.asarray(a[n]), np.asarray(b[n])
+        if x.dtype.kind == "f":
+            assert np.array_equal(x.view(np.uint32), y.view(np.uint32)), f"{label}: {n} differs"
+        else:
+            assert np.array_equal(x, y), f"{label}: {n} differs"
+
+
+def _graph_kernel_nodes(fn) -> int:
+    """Kernel launches of fn(), captured into a HIP graph and counted."""
+    g = torch.cuda.CUDAGraph(keep_graph=True)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        fn()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    with torch.cuda.graph(g):
+        fn()
+    hip = ctypes.CDLL("libamdhip64.so")
+    n = ctypes.c_size_t(0)
+    assert hip.hipGraphGetNodes(ctypes.c_void_p(g.raw_cuda_graph()), None, ctypes.byref(n)) == 0
+    return int(n.value)
+
+
+@pytest.mark.parametrize("packed", [False, True])
+@pytest.mark.parametrize("label,shape,B,fused", CASES, ids=[c[0] for c in CASES])
+def test_moe_layer_equals_four_calls(label, shape, B, fused, packed):
+    if packed and shape.wdt == "f32":
+        pytest.skip("fp32 weights are not packed")
+    d = make_inputs(shape, B, seed=31 + B + shape.n_experts, rho=0.5)
+    tag = f"{label} packed={packed}"
+    log(f"[moe_layer] {tag}: H={shape.hidden} F={shape.ffn} E={shape.n_experts} "
+        f"k={shape.top_k} S={shape.n_shared} B={B} wdt={shape.wdt}")
+    p1, ins, w, _dev1 = _run(shape, d, fused=True, packed=packed)
+    p4, _, _, _dev4 = _run(shape, d, fused=False, packed=packed)
+    got1, got4 = p1.results(), p4.results()
+    _assert_same(got1, got4, tag)
+    if fused:
+        ref = oracle.forward(d["x"], d["router"], d["conf_w"], d["experts"], d["shared"], shape)
+        check_routing(got1, ref, tag)
+        check_outputs(got1, ref, shape.wdt, tag)
+    log(f"[moe_layer] {tag}: equal, n_uniq={got1['n_uniq']}")
+
+
+@pytest.mark.parametrize("label,shape,B,fused", [CASES[1], CASES[2], CASES[8], CASES[12]],
+                         ids=[CASES[i][0] for i in (1, 2, 8, 12)])
+def test_moe_layer_launch_count(label, shape, B, fused):
+    import paper_2608_15018_amd as s2
+    d = make_inputs(shape, B, seed=5, rho=0.5)
+    p1, ins, w, _dev = _run(shape, d, fused=True, packed=True)
+    n1 = _graph_kernel_nodes(lambda: p1(*ins, w))
+    p4 = s2.VerifyPass(p1.layer, B, fused=False)
+    n4 = _graph_kernel_nodes(lambda: p4(*ins, w))
+    log(f"[moe_layer] {label}: {n1} launches in one call, {n4} as four calls")
+    if fused:
+        assert n1 == 3 and n4 == 6, (n1, n4)
+    else:
+        assert n1 == n4, (n1, n4)
+
+
+def test_moe_layer_graph_replays():
+    """Replays of a captured fused call, with eager work and
+    synchronisations in between, equal the eager call bit for bit."""
+    shape = CASES[2][1]
+    d = make_inputs(shape, 3, seed=77, rho=0.5)
+    p, ins, w, _dev = _run(shape, d, fused=True, packed=True)
+    eager = p.results()
+    g = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        p(*ins, w)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    with torch.cuda.graph(g):
+        p(*ins, w)
+    for rep in range(3):
+        _poison(p)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        _assert_same(p.results(), eager, f"replay {rep}")
+        p(*ins, w)
+        torch.cuda.synchronize()
+    log("[moe_layer] graph replays equal the eager call")
