@@ -223,10 +223,12 @@ __global__ __launch_bounds__(W * 64) void ffn_bf16_kernel(FfnArgs a) {
 // compute, so the results are the same bit for bit.
 
 // Gate-up with the routing in its prologue: wave 0 of every workgroup ranks
-// each token's logits and gates the batch (wave_select_plain, small_gate:
-// the code of the routing and gating kernels), leaving the buckets in LDS;
-// workgroup 0 also writes every routing output to global memory.  The unit
-// work is ffn_bf16_kernel<0, ...>'s, resolved from the LDS buckets.
+// each token's logits (wave_select_plain, the routing kernel's code) and
+// buckets the B k assignments in registers (lane_buckets), leaving the
+// buckets in LDS.  One extra workgroup, the last, instead runs small_gate
+// (the gating kernel's code: g, E*, gate weights, buckets), writes every
+// routing output to global memory and exits.  The unit work of the others is
+// ffn_bf16_kernel<0, ...>'s, resolved from the LDS buckets.
 template <int NJ, int TMAX, int R, int W, int U, bool kPacked>
 __global__ __launch_bounds__(W * 64) void ffn_bf16_gate_up_routed_kernel(FfnArgs a,
                                                                         RouteArgs ra,
@@ -234,15 +236,30 @@ __global__ __launch_bounds__(W * 64) void ffn_bf16_gate_up_routed_kernel(FfnArgs
   __shared__ SmallGateLds rt;
   __shared__ f32x4 red[W > 1 ? W * 2 * R * TMAX * kWave : 1];
   if (wave_id() == 0) {
-    const bool pub = blockIdx.x == 0;
+    const bool pub = blockIdx.x == gridDim.x - 1;
     for (int b = 0; b < ga.B; ++b)
       wave_select_plain<NJ>(ra.E, ra.k, ra.logits + (size_t)b * ra.E, rt.plain + b * ra.k,
                             rt.gap + b, pub ? ra.plain_idx + (size_t)b * ra.k : nullptr,
                             pub ? ra.gap + b : nullptr);
     wave_sync();
-    small_gate<NJ>(ga, rt.plain, rt.gap, rt, pub);
+    if (pub) {
+      small_gate<NJ>(ga, rt.plain, rt.gap, rt, true);
+    } else {
+      const int lane = threadIdx.x, n = ga.B * ga.k;
+      const int e = lane < n ? rt.plain[lane] : 0;
+      const LaneBuckets lb = lane_buckets(e, n);
+      if (lane < n) rt.slot[lb.less + lb.before] = lane;
+      if (lb.first) {
+        rt.uniq[lb.distinct_less] = e;
+        rt.count[e] = lb.count;
+        rt.offset[e] = lb.less;
+      }
+      const int nu = __popcll(__ballot(lb.first));
+      if (lane == 0) rt.n_uniq = nu;
+    }
   }
   __syncthreads();
+  if (blockIdx.x == gridDim.x - 1) return;
   FfnArgs b = a;
   b.count = rt.count;
   b.offset = rt.offset;
@@ -257,46 +274,56 @@ constexpr int kSmallOutRows = kSmallMaxTokens * kMaxTopK + kMaxShared * kSmallMa
 
 // Down projection and combine in one launch.  A workgroup takes 16 R rows of
 // H for every segment (the shared experts, then the activated experts in
-// uniq order); wave w works on segment w / KW over K part w % KW, the K
+// ascending id); wave w works on segment w / KW over K part w % KW, the K
 // ranges and the order in which the parts are added being those of the down
-// kernel with KW waves.  The segment's tile goes to expert_out as there and
-// to LDS, and the workgroup then forms y for its rows with the combine
-// kernel's arithmetic (the k routed terms as fmaf in slot order, then the
-// shared terms).
+// kernel with KW waves.  Each wave finds its segment from the published
+// top-k (`idx`, one id per lane, bucketed in registers by lane_buckets: the
+// same buckets the gating step published), so that one load of the routing
+// precedes the weight stream.  The segment's tile goes to expert_out as in
+// the down kernel and to LDS, and the workgroup then forms y for its rows
+// with the combine kernel's arithmetic (the k routed terms as fmaf in slot
+// order, then the shared terms).
 template <int R, int KW, int U, bool kPacked>
 __global__ __launch_bounds__(1024) void ffn_bf16_down_combine_kernel(FfnArgs a,
+                                                                     const int32_t* idx,
                                                                      const float* gate_w,
                                                                      float* y) {
   constexpr int kRows = 16 * R;
   __shared__ f32x4 red[16 * R * kWave];
   __shared__ float eo_s[kSmallOutRows][kRows];
+  __shared__ float gw_s[kWave];
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = wave_id();
   const int rA = lane & 15, gK = lane >> 4;
   const int seg_i = wave / KW, part = wave - seg_i * KW;
   const int r0 = blockIdx.x * kRows;
-  const int slots = min(a.E, a.B * a.k);
+  const int n_asg = a.B * a.k;
 
-  // Segment of this wave; the same checks as resolve_block.
+  // The batch's assignments and gate weights, one per lane; ids outside
+  // [0, E) (routing never computed) are clamped so nothing is addressed out
+  // of range.
+  const int e_l = lane < n_asg ? min(max(idx[lane], 0), a.E - 1) : 0;
+  const float gw_l = lane < n_asg ? gate_w[lane] : 0.f;
+  if (wave == 0) gw_s[lane] = gw_l;
+
   Segment seg;
   bool live = false;
+  uint64_t members = 0;
   if (seg_i < a.S) {
     seg.shared = true;
     seg.id = seg_i;
     seg.n = a.B;
-    seg.base = a.B * a.k + seg_i * a.B;
+    seg.base = n_asg + seg_i * a.B;
     live = true;
   } else {
-    const int u = seg_i - a.S;
-    if (u < min(*a.n_uniq, slots)) {
-      const int e = a.uniq[u];
-      if (e >= 0 && e < a.E) {
-        seg.shared = false;
-        seg.id = e;
-        seg.n = a.count[e];
-        seg.base = a.offset[e];
-        live = seg.n > 0 && seg.base >= 0 && seg.base + seg.n <= a.B * a.k;
-      }
+    const LaneBuckets lb = lane_buckets(e_l, n_asg);
+    int e = 0, cnt = 0, off = 0;
+    if (lane_bucket_segment(e_l, n_asg, lb, seg_i - a.S, &e, &cnt, &off, &members)) {
+      seg.shared = false;
+      seg.id = e;
+      seg.n = cnt;
+      seg.base = off;
+      live = true;
     }
   }
 
@@ -344,7 +371,7 @@ __global__ __launch_bounds__(1024) void ffn_bf16_down_combine_kernel(FfnArgs a,
       }
     }
     if (rA < seg.n) {
-      const int row = out_row(a, seg, rA);
+      const int row = seg.shared ? seg.base + rA : nth_set_bit(members, rA);
       float* dst = a.out + (size_t)row * a.H;
 #pragma unroll
       for (int r = 0; r < R; ++r) {
@@ -358,7 +385,7 @@ __global__ __launch_bounds__(1024) void ffn_bf16_down_combine_kernel(FfnArgs a,
   for (int i = threadIdx.x; i < a.B * kRows; i += blockDim.x) {
     const int b = i / kRows, c = i - b * kRows;
     float v = 0.f;
-    for (int j = 0; j < a.k; ++j) v = fmaf(gate_w[b * a.k + j], eo_s[b * a.k + j][c], v);
+    for (int j = 0; j < a.k; ++j) v = fmaf(gw_s[b * a.k + j], eo_s[b * a.k + j][c], v);
     for (int sh = 0; sh < a.S; ++sh) v += eo_s[a.B * a.k + sh * a.B + b][c];
     y[(size_t)b * a.H + r0 + c] = v;
   }
@@ -416,10 +443,10 @@ hipError_t launch_mode(const FfnArgs& a, int spw, hipStream_t s) {
 #define S2MOE_BF16_LARGE 4, 2, 1, 4, 1, 16
 #endif
 
-template <int TMAX, int RG, int UG, int RD, int UD, int SPW>
+template <int TMAX, int RG, int UG, int RD, int UD, int SPW, int SPWD = SPW>
 hipError_t launch_bf16_pair(const FfnArgs& a, hipStream_t s) {
   hipError_t err = launch_mode<0, TMAX, RG, UG>(a, SPW, s);
-  return err != hipSuccess ? err : launch_mode<1, TMAX, RD, UD>(a, SPW, s);
+  return err != hipSuccess ? err : launch_mode<1, TMAX, RD, UD>(a, SPWD, s);
 }
 
 // The fused small-batch layer with the tiny-batch configuration above: the
@@ -427,13 +454,13 @@ hipError_t launch_bf16_pair(const FfnArgs& a, hipStream_t s) {
 // launches take, so the arithmetic is the same.
 constexpr int kFusedMaxWaves = 16;
 
-template <int TMAX, int RG, int UG, int RD, int UD, int SPW>
+template <int TMAX, int RG, int UG, int RD, int UD, int SPW, int SPWD = SPW>
 struct SmallLayer {
   static_assert(TMAX == 1, "one token tile");
   static int down_waves(const FfnArgs& a) {
     int nks = a.F / 32;
     if (a.S > 0) nks = min(nks, a.Fs / 32);
-    return pick_waves(nks, RD * TMAX, SPW);
+    return pick_waves(nks, RD * TMAX, SPWD);
   }
   static bool fits(const FfnArgs& a) {
     return (a.S + min(a.E, a.B * a.k)) * down_waves(a) <= kFusedMaxWaves;
@@ -443,7 +470,7 @@ struct SmallLayer {
   static hipError_t gate_up(const FfnArgs& a, const RouteArgs& ra, const GateArgs& ga,
                             hipStream_t s) {
     const int w = pick_waves(a.H / 32, 2 * RG * TMAX, SPW);
-    const dim3 grid(n_blocks(a, 0, 16 * RG));
+    const dim3 grid(n_blocks(a, 0, 16 * RG) + 1);
     switch (w) {
       case 1: hipLaunchKernelGGL((ffn_bf16_gate_up_routed_kernel<NJ, TMAX, RG, 1, UG, kPacked>), grid, dim3(64), 0, s, a, ra, ga); break;
       case 2: hipLaunchKernelGGL((ffn_bf16_gate_up_routed_kernel<NJ, TMAX, RG, 2, UG, kPacked>), grid, dim3(128), 0, s, a, ra, ga); break;
@@ -454,15 +481,16 @@ struct SmallLayer {
   }
 
   template <bool kPacked>
-  static hipError_t down(const FfnArgs& a, const float* gate_w, float* y, hipStream_t s) {
+  static hipError_t down(const FfnArgs& a, const int32_t* idx, const float* gate_w, float* y,
+                         hipStream_t s) {
     const int kw = down_waves(a);
     const dim3 grid(a.H / (16 * RD));
     const dim3 block(64 * kw * (a.S + min(a.E, a.B * a.k)));
     switch (kw) {
-      case 1: hipLaunchKernelGGL((ffn_bf16_down_combine_kernel<RD, 1, UD, kPacked>), grid, block, 0, s, a, gate_w, y); break;
-      case 2: hipLaunchKernelGGL((ffn_bf16_down_combine_kernel<RD, 2, UD, kPacked>), grid, block, 0, s, a, gate_w, y); break;
-      case 4: hipLaunchKernelGGL((ffn_bf16_down_combine_kernel<RD, 4, UD, kPacked>), grid, block, 0, s, a, gate_w, y); break;
-      default: hipLaunchKernelGGL((ffn_bf16_down_combine_kernel<RD, 8, UD, kPacked>), grid, block, 0, s, a, gate_w, y); break;
+      case 1: hipLaunchKernelGGL((ffn_bf16_down_combine_kernel<RD, 1, UD, kPacked>), grid, block, 0, s, a, idx, gate_w, y); break;
+      case 2: hipLaunchKernelGGL((ffn_bf16_down_combine_kernel<RD, 2, UD, kPacked>), grid, block, 0, s, a, idx, gate_w, y); break;
+      case 4: hipLaunchKernelGGL((ffn_bf16_down_combine_kernel<RD, 4, UD, kPacked>), grid, block, 0, s, a, idx, gate_w, y); break;
+      default: hipLaunchKernelGGL((ffn_bf16_down_combine_kernel<RD, 8, UD, kPacked>), grid, block, 0, s, a, idx, gate_w, y); break;
     }
     return hipGetLastError();
   }
@@ -476,7 +504,7 @@ struct SmallLayer {
     else if (a.E <= 128) err = gate_up<2, kPacked>(a, ra, ga, s);
     else err = gate_up<4, kPacked>(a, ra, ga, s);
     if (err != hipSuccess) return err;
-    return down<kPacked>(a, ga.gate_w, y, s);
+    return down<kPacked>(a, ga.idx, ga.gate_w, y, s);
   }
 };
 

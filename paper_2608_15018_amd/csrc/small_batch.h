@@ -96,27 +96,30 @@ struct SmallGateLds {
 // same lambda).  One wave computes g and E* as the workgroup gating kernel
 // does (same runs of tokens, same ranking order), takes the plain top-k
 // (`plain` [B k], `gap_in` [B]: global or LDS), forms the gate weights with
-// the same arithmetic and buckets the B k assignments.  publish: also write
-// every output of the gating step to a's global arrays (the bucketing is
-// always left in s).
+// the same arithmetic and buckets the B k assignments.  publish: also
+// compute g, E* and the gate weights and write every output of the gating
+// step to a's global arrays; without it only the bucketing is computed (it
+// is always left in s).
 template <int kNJ>
 __device__ __forceinline__ void small_gate(const GateArgs& a, const int32_t* plain,
                                            const float* gap_in, SmallGateLds& s, bool publish) {
   const int lane = threadIdx.x & (kWave - 1);
   const int B = a.B, E = a.E, k = a.k, n_asg = B * k;
 
-  // Every global read is issued up front: confidences, gaps, the plain top-k
-  // and all B x E logits (at most 4 x 4 per lane).
+  // Every global read is issued up front: confidences, gaps and all B x E
+  // logits (at most 4 x 4 per lane; only g, E* and the gate weights need
+  // them), and the plain top-k.
   float w[kSmallMaxTokens], gap[kSmallMaxTokens], lg[kSmallMaxTokens][kNJ];
   int active = 0;
 #pragma unroll
   for (int b = 0; b < kSmallMaxTokens; ++b) {
-    w[b] = b < B ? fmaxf(a.conf_w[b], 0.f) : 0.f;
-    gap[b] = b < B ? gap_in[b] : 0.f;
+    const bool use = publish && b < B;
+    w[b] = use ? fmaxf(a.conf_w[b], 0.f) : 0.f;
+    gap[b] = use ? gap_in[b] : 0.f;
 #pragma unroll
     for (int j = 0; j < kNJ; ++j) {
       const int e = lane + kWave * j;
-      lg[b][j] = b < B && e < E ? a.logits[(size_t)b * E + e] : 0.f;
+      lg[b][j] = use && e < E ? a.logits[(size_t)b * E + e] : 0.f;
     }
     active |= w[b] > 0.f;
   }
@@ -142,44 +145,45 @@ __device__ __forceinline__ void small_gate(const GateArgs& a, const int32_t* pla
   }
   wave_sync();
 
-  // g_e in the same runs of tokens as the workgroup kernel.
-  int parts = 1;
-  while (parts * 2 * E <= 1024 && parts * 2 <= B) parts *= 2;
-  const int run = (B + parts - 1) / parts;
-  uint32_t key[1][kNJ];
-  int n_cand = 0;
-#pragma unroll
-  for (int j = 0; j < kNJ; ++j) {
-    const int e = lane + kWave * j;
-    key[0][j] = 0;
-    if (e < E) {
-      float tot = 0.f;
-      for (int part = 0; part < parts; ++part) {
-        float sum = 0.f;
-#pragma unroll
-        for (int b = 0; b < kSmallMaxTokens; ++b)
-          if (b >= part * run && b < min(B, part * run + run)) sum = fmaf(w[b], lg[b][j], sum);
-        tot = part == 0 ? sum : tot + sum;
-      }
-      if (publish) a.g[e] = tot;
-      if (s.cand[e]) key[0][j] = order_key(tot);
-    }
-    n_cand += __popcll(__ballot(e < E && s.cand[e]));
-  }
-  // E* = the cap candidates of largest g (ties: lower id).
+  // g_e in the same runs of tokens as the workgroup kernel, and E* (only
+  // the published outputs and the gate weights need them).
   uint32_t pref_bits = 0;
-  if (active) {
-    if (n_cand <= a.cap) {
-#pragma unroll
-      for (int j = 0; j < kNJ; ++j)
-        if (key[0][j] != 0) pref_bits |= 1u << j;
-    } else {
-      uint32_t sel[1];
-      wave_top_k<1, kNJ>(key, a.cap, sel);
-      pref_bits = sel[0];
-    }
-  }
   if (publish) {
+    int parts = 1;
+    while (parts * 2 * E <= 1024 && parts * 2 <= B) parts *= 2;
+    const int run = (B + parts - 1) / parts;
+    uint32_t key[1][kNJ];
+    int n_cand = 0;
+#pragma unroll
+    for (int j = 0; j < kNJ; ++j) {
+      const int e = lane + kWave * j;
+      key[0][j] = 0;
+      if (e < E) {
+        float tot = 0.f;
+        for (int part = 0; part < parts; ++part) {
+          float sum = 0.f;
+#pragma unroll
+          for (int b = 0; b < kSmallMaxTokens; ++b)
+            if (b >= part * run && b < min(B, part * run + run)) sum = fmaf(w[b], lg[b][j], sum);
+          tot = part == 0 ? sum : tot + sum;
+        }
+        a.g[e] = tot;
+        if (s.cand[e]) key[0][j] = order_key(tot);
+      }
+      n_cand += __popcll(__ballot(e < E && s.cand[e]));
+    }
+    // E* = the cap candidates of largest g (ties: lower id).
+    if (active) {
+      if (n_cand <= a.cap) {
+#pragma unroll
+        for (int j = 0; j < kNJ; ++j)
+          if (key[0][j] != 0) pref_bits |= 1u << j;
+      } else {
+        uint32_t sel[1];
+        wave_top_k<1, kNJ>(key, a.cap, sel);
+        pref_bits = sel[0];
+      }
+    }
 #pragma unroll
     for (int j = 0; j < kNJ; ++j) {
       const int e = lane + kWave * j;
@@ -278,6 +282,60 @@ __device__ __forceinline__ void small_gate(const GateArgs& a, const int32_t* pla
     s.slot[s.offset[my_e] + before] = lane;
     if (publish) a.slot[s.offset[my_e] + before] = lane;
   }
+}
+
+// Buckets of n <= 64 assignments held one per lane (lane i < n holds the
+// expert e_i of assignment i), computed in registers by uniform loops over
+// the n lanes: the same bucketing as small_gate (experts in ascending id,
+// each expert's assignments in assignment order).
+struct LaneBuckets {
+  int less;           // assignments to experts below e_i: offset[e_i]
+  int before;         // earlier assignments to e_i: slot[less + before] = i
+  int count;          // assignments to e_i: count[e_i]
+  int distinct_less;  // activated experts below e_i: e_i = uniq[distinct_less]
+  bool first;         // i is e_i's first assignment
+};
+
+__device__ __forceinline__ LaneBuckets lane_buckets(int e, int n) {
+  const int lane = threadIdx.x & (kWave - 1);
+  LaneBuckets b{0, 0, 0, 0, false};
+  for (int j = 0; j < n; ++j) {
+    const int ej = __builtin_amdgcn_readlane(e, j);
+    b.less += ej < e;
+    b.count += ej == e;
+    b.before += ej == e && j < lane;
+  }
+  b.first = lane < n && b.before == 0;
+  uint64_t m = __ballot(b.first);
+  while (m) {
+    const int j = __builtin_ctzll(m);
+    m &= m - 1;
+    b.distinct_less += __builtin_amdgcn_readlane(e, j) < e;
+  }
+  return b;
+}
+
+// Segment u of the buckets (the u-th activated expert in ascending id):
+// false when fewer experts are activated; else its expert, assignment count
+// and offset, and the mask of its assignments (lanes), in order.
+__device__ __forceinline__ bool lane_bucket_segment(int e, int n, const LaneBuckets& b, int u,
+                                                    int* e_u, int* count, int* offset,
+                                                    uint64_t* members) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const uint64_t m = __ballot(b.first && b.distinct_less == u);
+  if (m == 0) return false;
+  const int l = __builtin_ctzll(m);
+  *e_u = __builtin_amdgcn_readlane(e, l);
+  *count = __builtin_amdgcn_readlane(b.count, l);
+  *offset = __builtin_amdgcn_readlane(b.less, l);
+  *members = __ballot(lane < n && e == *e_u);
+  return true;
+}
+
+// Index of the t-th set bit of m (t < popcount(m)).
+__device__ __forceinline__ int nth_set_bit(uint64_t m, int t) {
+  for (int i = 0; i < t; ++i) m &= m - 1;
+  return __builtin_ctzll(m);
 }
 
 }  // namespace s2moe
