@@ -459,7 +459,7 @@ def bench_stack(args, wl, shape, B: int, wid: int) -> int:
         dev, w = s2.pack_expert_weights((ex, sh), shape.wdt)
         del ex, sh
         keep.append(dev)
-        passes.append(s2.VerifyPass(layer, B))
+        passes.append(s2.VerifyPass(layer, B, fused=True))
         ins.append((s2.to_device(x), s2.to_device(router), s2.to_device(conf_w), w))
     torch.cuda.synchronize()
     _log(f"[bench] {wl.name}: {L} layers generated and packed in {time.time() - t0:.1f}s")
@@ -619,7 +619,8 @@ def bench_layer(args, wl, shape, B: int, default_B: int, wid: int, stream_ref: b
     # verify step then streams each activated expert's tiles contiguously.
     packed = shape.wdt != "f32" and not args.plain_weights
     layer = s2.make_layer(shape, flags=shape.flags | (s2.PACKED_WEIGHTS if packed else 0))
-    p = s2.VerifyPass(layer, B)
+    p = s2.VerifyPass(layer, B, fused=True)
+    p4 = s2.VerifyPass(layer, B, fused=False)
     xd, rd, cd = s2.to_device(x), s2.to_device(router), s2.to_device(conf_w)
     dev_w, wstruct = s2.weights_to_device(experts, shared)
     if packed:
@@ -635,7 +636,8 @@ def bench_layer(args, wl, shape, B: int, default_B: int, wid: int, stream_ref: b
     unique_bytes = n_uniq * expert_bytes(shape, shape.ffn) + \
         shape.n_shared * expert_bytes(shape, shape.ffn_shared)
 
-    # Timed region 1: K whole steps back to back (no host sync, no events).
+    # Timed region 1: K whole steps back to back (no host sync, no events),
+    # each one s2moe_moe_layer call; then the same steps as the four calls.
     torch.cuda.synchronize()
     t_start = time.perf_counter()
     for _ in range(args.steps):
@@ -643,6 +645,13 @@ def bench_layer(args, wl, shape, B: int, default_B: int, wid: int, stream_ref: b
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t_start
     ms_per_step = elapsed / args.steps * 1e3
+    p4(xd, rd, cd, wstruct)
+    torch.cuda.synchronize()
+    t4 = time.perf_counter()
+    for _ in range(args.steps):
+        p4(xd, rd, cd, wstruct)
+    torch.cuda.synchronize()
+    four_call_ms = (time.perf_counter() - t4) / args.steps * 1e3
 
     # Timed region 2: K back-to-back s2moe_verify_moe calls between one pair
     # of HIP events on the launch stream (an event pair costs a few
@@ -719,6 +728,8 @@ def bench_layer(args, wl, shape, B: int, default_B: int, wid: int, stream_ref: b
         "n_uniq": n_uniq,
         "reuse_ratio": n_uniq / (B * shape.top_k),
         "ffn_timing": ffn_note,
+        "step": "one s2moe_moe_layer call (route, gate, experts, combine)",
+        "four_call_ms_per_step": four_call_ms,
     }
     if stream_gbs is not None:
         out["stream_read"] = {"value": stream_gbs, "unit": "GB/s",

@@ -614,8 +614,7 @@ s2moe_status s2moe_moe_layer(const s2moe_layer* layer, int32_t n_tokens, const v
   const hipStream_t s = static_cast<hipStream_t>(stream);
   if (s2moe::moe_layer_small_fits(fa, layer->alpha))
     return hip_status(fn, s2moe::launch_moe_layer_small(ra, ga, fa, y, s));
-  hipError_t err = s2moe::launch_route(ra, s);
-  if (err == hipSuccess) err = s2moe::launch_reuse_gate(ga, s);
+  hipError_t err = s2moe::launch_route_and_gate(ra, ga, s);
   if (err == hipSuccess) err = s2moe::launch_ffn(fa, s);
   if (err == hipSuccess) err = s2moe::launch_combine(ca, s);
   return hip_status(fn, err);

@@ -237,14 +237,8 @@ __global__ __launch_bounds__(W * 64) void ffn_bf16_gate_up_routed_kernel(FfnArgs
   __shared__ f32x4 red[W > 1 ? W * 2 * R * TMAX * kWave : 1];
   if (wave_id() == 0) {
     const bool pub = blockIdx.x == gridDim.x - 1;
-    for (int b = 0; b < ga.B; ++b)
-      wave_select_plain<NJ>(ra.E, ra.k, ra.logits + (size_t)b * ra.E, rt.plain + b * ra.k,
-                            rt.gap + b, pub ? ra.plain_idx + (size_t)b * ra.k : nullptr,
-                            pub ? ra.gap + b : nullptr);
-    wave_sync();
-    if (pub) {
-      small_gate<NJ>(ga, rt.plain, rt.gap, rt, true);
-    } else {
+    small_route_gate<NJ>(ra, ga, rt, pub);
+    if (!pub) {
       const int lane = threadIdx.x, n = ga.B * ga.k;
       const int e = lane < n ? rt.plain[lane] : 0;
       const LaneBuckets lb = lane_buckets(e, n);

@@ -24,9 +24,14 @@ namespace s2moe {
 constexpr int kStage = 10240;  // logits staged in LDS up to B * E = 10240
 
 // kNJ = expert slots per lane (E <= 64 kNJ); kNT = tokens a wave takes
-// through the threshold search together.
-template <bool kStaged, int kNJ, int kNT>
-__global__ __launch_bounds__(1024) void reuse_gate_kernel(GateArgs a) {
+// through the threshold search together.  kSelect (with kStaged): the
+// kernel first ranks every token's staged logits itself (wave_select_plain,
+// the routing kernel's code, one wave per token) and writes plain_idx and
+// gap, instead of reading them from a routing launch (ra: the routing
+// step's arguments).
+template <bool kStaged, int kNJ, int kNT, bool kSelect>
+__global__ __launch_bounds__(1024) void reuse_gate_kernel(GateArgs a, RouteArgs ra) {
+  static_assert(kStaged || !kSelect, "ranking reads the staged logits");
   constexpr int kMaskWords = kMaxTokens / 64;
   __shared__ float ell_s[kStaged ? kStage : 1];
   __shared__ float w_s[kMaxTokens];
@@ -42,6 +47,7 @@ __global__ __launch_bounds__(1024) void reuse_gate_kernel(GateArgs a) {
   __shared__ float gpart_s[1024];
   uint8_t* idx_s = reinterpret_cast<uint8_t*>(gpart_s);
   __shared__ int cand_s[kMaxExperts];
+  __shared__ uint8_t plain_s[kSelect ? kMaxTokens * kMaxTopK : 1];
 
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
@@ -54,7 +60,7 @@ __global__ __launch_bounds__(1024) void reuse_gate_kernel(GateArgs a) {
   if (tid < B) {
     const float w = fmaxf(a.conf_w[tid], 0.f);
     w_s[tid] = w;
-    gap_s[tid] = a.gap[tid];
+    if (!kSelect) gap_s[tid] = a.gap[tid];
     positive = w > 0.f;
   }
   if (kStaged) {
@@ -81,10 +87,17 @@ __global__ __launch_bounds__(1024) void reuse_gate_kernel(GateArgs a) {
   const int active = __syncthreads_or(positive);
   const float* ell = kStaged ? static_cast<const float*>(ell_s) : a.logits;
 
+  if (kSelect) {
+    for (int b = wave; b < B; b += n_waves)
+      wave_select_plain<kNJ>(E, k, ell + (size_t)b * E, plain_s + b * k, gap_s + b,
+                             ra.plain_idx + (size_t)b * k, ra.gap + b);
+    __syncthreads();
+  }
+
   // TopCap candidates: all experts, or those in some token's plain top-k.
   if (a.flags & kPrefActivatedOnly) {
     for (int i = tid; i < B * k; i += blockDim.x) {
-      const int e = a.plain_idx[i];
+      const int e = kSelect ? (int)plain_s[i] : a.plain_idx[i];
       if (e >= 0 && e < E) cand_s[e] = 1;
     }
   }
@@ -269,28 +282,40 @@ __global__ __launch_bounds__(kWave) void reuse_gate_small_kernel(GateArgs a) {
   small_gate<kNJ>(a, a.plain_idx, a.gap, s, true);
 }
 
-template <bool kStaged, int kNJ>
-void launch_gate_nj(const GateArgs& a, hipStream_t s) {
-  if (a.B <= 16)
-    hipLaunchKernelGGL((reuse_gate_kernel<kStaged, kNJ, 1>), dim3(1), dim3(1024), 0, s, a);
-  else if (a.B <= 32)
-    hipLaunchKernelGGL((reuse_gate_kernel<kStaged, kNJ, 2>), dim3(1), dim3(1024), 0, s, a);
-  else
-    hipLaunchKernelGGL((reuse_gate_kernel<kStaged, kNJ, 4>), dim3(1), dim3(1024), 0, s, a);
+// The same, ranking the tokens' logits first (small_route_gate): the
+// routing launch's ranking and this gating in one single-wave launch.
+template <int kNJ>
+__global__ __launch_bounds__(kWave) void route_gate_small_kernel(RouteArgs ra, GateArgs a) {
+  __shared__ SmallGateLds s;
+  small_route_gate<kNJ>(ra, a, s, true);
 }
 
-template <bool kStaged>
-void launch_gate_staged(const GateArgs& a, hipStream_t s) {
-  if (a.E <= 64)
-    launch_gate_nj<kStaged, 1>(a, s);
-  else if (a.E <= 128)
-    launch_gate_nj<kStaged, 2>(a, s);
+template <bool kStaged, int kNJ, bool kSelect>
+void launch_gate_nj(const GateArgs& a, const RouteArgs& ra, hipStream_t s) {
+  if (a.B <= 16)
+    hipLaunchKernelGGL((reuse_gate_kernel<kStaged, kNJ, 1, kSelect>), dim3(1), dim3(1024), 0, s, a, ra);
+  else if (a.B <= 32)
+    hipLaunchKernelGGL((reuse_gate_kernel<kStaged, kNJ, 2, kSelect>), dim3(1), dim3(1024), 0, s, a, ra);
   else
-    launch_gate_nj<kStaged, 4>(a, s);
+    hipLaunchKernelGGL((reuse_gate_kernel<kStaged, kNJ, 4, kSelect>), dim3(1), dim3(1024), 0, s, a, ra);
+}
+
+template <bool kStaged, bool kSelect>
+void launch_gate_staged(const GateArgs& a, const RouteArgs& ra, hipStream_t s) {
+  if (a.E <= 64)
+    launch_gate_nj<kStaged, 1, kSelect>(a, ra, s);
+  else if (a.E <= 128)
+    launch_gate_nj<kStaged, 2, kSelect>(a, ra, s);
+  else
+    launch_gate_nj<kStaged, 4, kSelect>(a, ra, s);
+}
+
+bool small_gate_applies(const GateArgs& a) {
+  return a.B <= kSmallMaxTokens && (a.alpha == 0.f || a.B == 1);
 }
 
 hipError_t launch_reuse_gate(const GateArgs& a, hipStream_t s) {
-  if (a.B <= kSmallMaxTokens && (a.alpha == 0.f || a.B == 1)) {
+  if (small_gate_applies(a)) {
     if (a.E <= 64)
       hipLaunchKernelGGL(reuse_gate_small_kernel<1>, dim3(1), dim3(kWave), 0, s, a);
     else if (a.E <= 128)
@@ -299,10 +324,31 @@ hipError_t launch_reuse_gate(const GateArgs& a, hipStream_t s) {
       hipLaunchKernelGGL(reuse_gate_small_kernel<4>, dim3(1), dim3(kWave), 0, s, a);
     return hipGetLastError();
   }
+  const RouteArgs none{};
   if (a.B * a.E <= kStage)
-    launch_gate_staged<true>(a, s);
+    launch_gate_staged<true, false>(a, none, s);
   else
-    launch_gate_staged<false>(a, s);
+    launch_gate_staged<false, false>(a, none, s);
+  return hipGetLastError();
+}
+
+hipError_t launch_route_and_gate(const RouteArgs& ra, const GateArgs& a, hipStream_t s) {
+  if (!route_ranks_separately(ra) || (!small_gate_applies(a) && a.B * a.E > kStage)) {
+    const hipError_t err = launch_route(ra, s);
+    return err != hipSuccess ? err : launch_reuse_gate(a, s);
+  }
+  const hipError_t err = launch_route_rows(ra, s);
+  if (err != hipSuccess) return err;
+  if (small_gate_applies(a)) {
+    if (a.E <= 64)
+      hipLaunchKernelGGL(route_gate_small_kernel<1>, dim3(1), dim3(kWave), 0, s, ra, a);
+    else if (a.E <= 128)
+      hipLaunchKernelGGL(route_gate_small_kernel<2>, dim3(1), dim3(kWave), 0, s, ra, a);
+    else
+      hipLaunchKernelGGL(route_gate_small_kernel<4>, dim3(1), dim3(kWave), 0, s, ra, a);
+  } else {
+    launch_gate_staged<true, true>(a, ra, s);
+  }
   return hipGetLastError();
 }
 

@@ -177,6 +177,13 @@ hipError_t launch_expand(const ExpandArgs& a, size_t lds_bytes, hipStream_t s);
 hipError_t launch_route(const RouteArgs& a, hipStream_t s);
 // Logits only (the first launch of launch_route's small-batch path).
 hipError_t launch_route_rows(const RouteArgs& a, hipStream_t s);
+// Whether launch_route computes the logits and ranks them in two launches
+// (launch_route_rows, then one wave per token).
+bool route_ranks_separately(const RouteArgs& a);
+// launch_route then launch_reuse_gate, with the same results bit for bit;
+// where the routing ranks in a launch of its own, the gating launch ranks
+// the logits itself instead (gate.hip).
+hipError_t launch_route_and_gate(const RouteArgs& ra, const GateArgs& a, hipStream_t s);
 hipError_t launch_stream_read(const void* src, size_t bytes, uint32_t* sink, int blocks,
                               hipStream_t s);
 hipError_t launch_pack(const PackArgs& a, hipStream_t s);

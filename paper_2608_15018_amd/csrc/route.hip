@@ -95,7 +95,7 @@ template <int NJ>
 __global__ __launch_bounds__(kWave) void route_select_wave_kernel(RouteArgs a) {
   const int b = blockIdx.x;
   wave_select_plain<NJ>(a.E, a.k, a.logits + (size_t)b * a.E, a.plain_idx + (size_t)b * a.k,
-                        a.gap + b, nullptr, nullptr);
+                        a.gap + b, static_cast<int32_t*>(nullptr), nullptr);
 }
 
 template <bool kBf16, int NJ>
@@ -136,8 +136,8 @@ __global__ __launch_bounds__(1024) void route_kernel(RouteArgs a) {
   }
   __syncthreads();
   if (wave == 0)
-    wave_select_plain<NJ>(E, a.k, ell_s, a.plain_idx + (size_t)b * a.k, a.gap + b, nullptr,
-                          nullptr);
+    wave_select_plain<NJ>(E, a.k, ell_s, a.plain_idx + (size_t)b * a.k, a.gap + b,
+                          static_cast<int32_t*>(nullptr), nullptr);
 }
 
 }  // namespace
@@ -163,8 +163,12 @@ hipError_t launch_route_rows(const RouteArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
+bool route_ranks_separately(const RouteArgs& a) {
+  return a.B <= S2MOE_ROUTE_ROWS_MAX_B || a.E > S2MOE_ROUTE_ROWS_MIN_E;
+}
+
 hipError_t launch_route(const RouteArgs& a, hipStream_t s) {
-  if (a.B <= S2MOE_ROUTE_ROWS_MAX_B || a.E > S2MOE_ROUTE_ROWS_MIN_E) {
+  if (route_ranks_separately(a)) {
     const hipError_t e = launch_route_rows(a, s);
     if (e != hipSuccess) return e;
     if (a.E <= 64)

@@ -30,9 +30,9 @@ __device__ __forceinline__ void wave_sync() {
 // member (smallest value, then largest id) is the (k+1)-th, the other k are
 // the plain top-k, written in id order to idx[0..k); gap = ell_(1) -
 // ell_(k+1) to *gap.  idx2 / gap2, when not null, get the same values.
-template <int NJ>
-__device__ __forceinline__ void wave_select_plain(int E, int k, const float* ell, int32_t* idx,
-                                                  float* gap, int32_t* idx2, float* gap2) {
+template <int NJ, class I1, class I2>
+__device__ __forceinline__ void wave_select_plain(int E, int k, const float* ell, I1* idx,
+                                                  float* gap, I2* idx2, float* gap2) {
   const int lane = threadIdx.x & (kWave - 1);
   uint32_t key[1][NJ];
 #pragma unroll
@@ -65,8 +65,8 @@ __device__ __forceinline__ void wave_select_plain(int E, int k, const float* ell
 #pragma unroll
   for (int j = 0; j < NJ; ++j)
     if ((bits >> j) & 1u) {
-      idx[rank[j]] = lane + kWave * j;
-      if (idx2) idx2[rank[j]] = lane + kWave * j;
+      idx[rank[j]] = (I1)(lane + kWave * j);
+      if (idx2) idx2[rank[j]] = (I2)(lane + kWave * j);
     }
   if (lane == 0) {
     const float gv = key_value(mx) - key_value(mn);
@@ -282,6 +282,23 @@ __device__ __forceinline__ void small_gate(const GateArgs& a, const int32_t* pla
     s.slot[s.offset[my_e] + before] = lane;
     if (publish) a.slot[s.offset[my_e] + before] = lane;
   }
+}
+
+// Plain top-k and gap of each of the B <= kSmallMaxTokens tokens
+// (wave_select_plain on the logits ra.logits) into s.plain / s.gap, and,
+// when publish, to ra.plain_idx / ra.gap; then, when publish, small_gate on
+// them (g, E*, gate weights, buckets, all written to ga's arrays).  One
+// wave; the results equal the routing kernel's ranking followed by the
+// single-wave gating kernel.
+template <int NJ>
+__device__ __forceinline__ void small_route_gate(const RouteArgs& ra, const GateArgs& ga,
+                                                 SmallGateLds& s, bool publish) {
+  for (int b = 0; b < ga.B; ++b)
+    wave_select_plain<NJ>(ra.E, ra.k, ra.logits + (size_t)b * ra.E, s.plain + b * ra.k,
+                          s.gap + b, publish ? ra.plain_idx + (size_t)b * ra.k : nullptr,
+                          publish ? ra.gap + b : nullptr);
+  wave_sync();
+  if (publish) small_gate<NJ>(ga, s.plain, s.gap, s, true);
 }
 
 // Buckets of n <= 64 assignments held one per lane (lane i < n holds the

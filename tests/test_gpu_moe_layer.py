@@ -8,7 +8,10 @@
   and row-major weights) and on batches that do not (alpha > 0 at B = 2,
   too many segments, B = 8, int4 and fp32 weights).
 * The number of launches, read from a captured HIP graph: 3 on the fused
-  path, 6 for the same layer as four calls.
+  path against 6 for the same layer as four calls; one fewer than the four
+  calls where the gating launch ranks the logits itself; the same count
+  where the routing ranks in its own workgroups or the logits are too many
+  to stage.
 * Against the oracle on the fused cases (routing exact, outputs within the
   bf16 tolerance), and graph replays equal to the eager call.
 """
@@ -59,6 +62,9 @@ CASES = [
     ("B8 (four calls)", _shape(), 8, False),
     ("int4 B2 (four calls)", _shape(wdt="q4g32"), 2, False),
     ("fp32 B1 (four calls)", _shape(act="f32", wdt="f32"), 1, False),
+    ("B16 E8 (route_kernel)", _shape(cap=4, alpha=0.5), 16, False),
+    ("B64 E256 (unstaged gate)", _shape(ffn=256, n_experts=256, top_k=4, cap=8, alpha=0.5), 64,
+     False),
 ]
 
 
@@ -131,20 +137,24 @@ def test_moe_layer_equals_four_calls(label, shape, B, fused, packed):
     log(f"[moe_layer] {tag}: equal, n_uniq={got1['n_uniq']}")
 
 
-@pytest.mark.parametrize("label,shape,B,fused", [CASES[1], CASES[2], CASES[8], CASES[12]],
-                         ids=[CASES[i][0] for i in (1, 2, 8, 12)])
-def test_moe_layer_launch_count(label, shape, B, fused):
+# (case, launches of one call, launches of the four calls).  Three on the
+# fused path; elsewhere the gating launch ranks the logits itself where the
+# routing would rank them in a launch of its own (B <= 8 or E > 64, logits
+# staged in LDS or a single-wave gate), and nothing changes otherwise.
+LAUNCHES = [(1, 3, 6), (2, 3, 6), (8, 5, 6), (12, 6, 7), (14, 5, 5), (15, 6, 6)]
+
+
+@pytest.mark.parametrize("case,n_call,n_four", LAUNCHES, ids=[CASES[c[0]][0] for c in LAUNCHES])
+def test_moe_layer_launch_count(case, n_call, n_four):
     import paper_2608_15018_amd as s2
+    label, shape, B, _fused = CASES[case]
     d = make_inputs(shape, B, seed=5, rho=0.5)
     p1, ins, w, _dev = _run(shape, d, fused=True, packed=True)
     n1 = _graph_kernel_nodes(lambda: p1(*ins, w))
     p4 = s2.VerifyPass(p1.layer, B, fused=False)
     n4 = _graph_kernel_nodes(lambda: p4(*ins, w))
     log(f"[moe_layer] {label}: {n1} launches in one call, {n4} as four calls")
-    if fused:
-        assert n1 == 3 and n4 == 6, (n1, n4)
-    else:
-        assert n1 == n4, (n1, n4)
+    assert (n1, n4) == (n_call, n_four)
 
 
 def test_moe_layer_graph_replays():
