@@ -135,30 +135,6 @@ __device__ __forceinline__ void wave_top_k(const uint32_t (&key)[NT][NJ], int k,
   }
 }
 
-// Ranks of n <= 1024 floats vals[0..n) in LDS by (value desc, index asc),
-// added into rank_s[0..n) (which the caller zeroes and fences first).  Each
-// element's comparisons are split over nthreads / n threads; the partial
-// counts meet through integer LDS atomics, so the ranks are exact and
-// independent of timing.  -0 and +0 compare equal.
-__device__ __forceinline__ void block_rank_desc(const float* vals, int n, int* rank_s, int tid,
-                                                int nthreads) {
-  int parts = 1;
-  while (parts * 2 * n <= nthreads) parts *= 2;
-  const int chunk = (n + parts - 1) / parts;
-  for (int i = tid; i < n * parts; i += nthreads) {
-    const int e = i / parts, part = i - e * parts;
-    const float v = vals[e];
-    const int lo = part * chunk, hi = min(n, lo + chunk);
-    int cnt = 0;
-#pragma unroll 8
-    for (int e2 = lo; e2 < hi; ++e2) {
-      const float v2 = vals[e2];
-      cnt += (v2 > v) || (v2 == v && e2 < e);
-    }
-    if (cnt) atomicAdd(&rank_s[e], cnt);
-  }
-}
-
 // Rank, in ascending expert id, of the flagged experts: expert lane + 64 j
 // with bit j set gets position rank[j].  Returns the number flagged.
 template <int NJ>
