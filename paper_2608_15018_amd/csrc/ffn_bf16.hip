@@ -12,8 +12,7 @@
 // A operand of v_mfma_f32_16x16x32_bf16: row = lane % 16, K slice =
 // lane / 16) and 16 bytes of each token tile (B operand, from the
 // L2-resident activations); the R row tiles share the token fragments.
-#include "ffn_common.h"
-#include "small_batch.h"
+#include "small_layer.h"
 
 namespace s2moe {
 
@@ -222,104 +221,40 @@ __global__ __launch_bounds__(W * 64) void ffn_bf16_kernel(FfnArgs a) {
 // two kernels below.  Each computes exactly what the unfused kernels
 // compute, so the results are the same bit for bit.
 
-// Gate-up with the routing in its prologue: wave 0 of every workgroup ranks
-// each token's logits (wave_select_plain, the routing kernel's code) and
-// buckets the B k assignments in registers (lane_buckets), leaving the
-// buckets in LDS.  One extra workgroup, the last, instead runs small_gate
-// (the gating kernel's code: g, E*, gate weights, buckets), writes every
-// routing output to global memory and exits.  The unit work of the others is
-// ffn_bf16_kernel<0, ...>'s, resolved from the LDS buckets.
+// Gate-up with the routing in its prologue (small_layer_routing): one extra
+// workgroup, the last, publishes the routing and exits; the unit work of the
+// others is ffn_bf16_kernel<0, ...>'s, resolved from the LDS buckets.
 template <int NJ, int TMAX, int R, int W, int U, bool kPacked>
 __global__ __launch_bounds__(W * 64) void ffn_bf16_gate_up_routed_kernel(FfnArgs a,
                                                                         RouteArgs ra,
                                                                         GateArgs ga) {
   __shared__ SmallGateLds rt;
   __shared__ f32x4 red[W > 1 ? W * 2 * R * TMAX * kWave : 1];
-  if (wave_id() == 0) {
-    const bool pub = blockIdx.x == gridDim.x - 1;
-    small_route_gate<NJ>(ra, ga, rt, pub);
-    if (!pub) {
-      const int lane = threadIdx.x, n = ga.B * ga.k;
-      const int e = lane < n ? rt.plain[lane] : 0;
-      const LaneBuckets lb = lane_buckets(e, n);
-      if (lane < n) rt.slot[lb.less + lb.before] = lane;
-      if (lb.first) {
-        rt.uniq[lb.distinct_less] = e;
-        rt.count[e] = lb.count;
-        rt.offset[e] = lb.less;
-      }
-      const int nu = __popcll(__ballot(lb.first));
-      if (lane == 0) rt.n_uniq = nu;
-    }
-  }
+  const bool pub = blockIdx.x == gridDim.x - 1;
+  if (wave_id() == 0) small_layer_routing<NJ>(ra, ga, rt, pub);
   __syncthreads();
-  if (blockIdx.x == gridDim.x - 1) return;
-  FfnArgs b = a;
-  b.count = rt.count;
-  b.offset = rt.offset;
-  b.slot = rt.slot;
-  b.uniq = rt.uniq;
-  b.n_uniq = &rt.n_uniq;
-  ffn_bf16_unit<0, TMAX, R, W, U, kPacked>(b, red);
+  if (pub) return;
+  ffn_bf16_unit<0, TMAX, R, W, U, kPacked>(with_lds_buckets(a, rt), red);
 }
 
-// Rows of expert_out a small batch can have: B k + S B.
-constexpr int kSmallOutRows = kSmallMaxTokens * kMaxTopK + kMaxShared * kSmallMaxTokens;
-
 // Down projection and combine in one launch.  A workgroup takes 16 R rows of
-// H for every segment (the shared experts, then the activated experts in
-// ascending id); wave w works on segment w / KW over K part w % KW, the K
-// ranges and the order in which the parts are added being those of the down
-// kernel with KW waves.  Each wave finds its segment from the published
-// top-k (`idx`, one id per lane, bucketed in registers by lane_buckets: the
-// same buckets the gating step published), so that one load of the routing
-// precedes the weight stream.  The segment's tile goes to expert_out as in
-// the down kernel and to LDS, and the workgroup then forms y for its rows
-// with the combine kernel's arithmetic (the k routed terms as fmaf in slot
-// order, then the shared terms).
+// H for every segment (small_down_segment); wave w works on segment w / KW
+// over K part w % KW with the down kernel's K ranges, and small_down_finish
+// adds the parts in the down kernel's order, writes expert_out and forms y.
 template <int R, int KW, int U, bool kPacked>
 __global__ __launch_bounds__(1024) void ffn_bf16_down_combine_kernel(FfnArgs a,
                                                                      const int32_t* idx,
                                                                      const float* gate_w,
                                                                      float* y) {
-  constexpr int kRows = 16 * R;
-  __shared__ f32x4 red[16 * R * kWave];
-  __shared__ float eo_s[kSmallOutRows][kRows];
-  __shared__ float gw_s[kWave];
+  __shared__ SmallDownLds<R> lds;
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = wave_id();
   const int rA = lane & 15, gK = lane >> 4;
   const int seg_i = wave / KW, part = wave - seg_i * KW;
-  const int r0 = blockIdx.x * kRows;
-  const int n_asg = a.B * a.k;
-
-  // The batch's assignments and gate weights, one per lane; ids outside
-  // [0, E) (routing never computed) are clamped so nothing is addressed out
-  // of range.
-  const int e_l = lane < n_asg ? min(max(idx[lane], 0), a.E - 1) : 0;
-  const float gw_l = lane < n_asg ? gate_w[lane] : 0.f;
-  if (wave == 0) gw_s[lane] = gw_l;
-
+  const int r0 = blockIdx.x * 16 * R;
   Segment seg;
-  bool live = false;
-  uint64_t members = 0;
-  if (seg_i < a.S) {
-    seg.shared = true;
-    seg.id = seg_i;
-    seg.n = a.B;
-    seg.base = n_asg + seg_i * a.B;
-    live = true;
-  } else {
-    const LaneBuckets lb = lane_buckets(e_l, n_asg);
-    int e = 0, cnt = 0, off = 0;
-    if (lane_bucket_segment(e_l, n_asg, lb, seg_i - a.S, &e, &cnt, &off, &members)) {
-      seg.shared = false;
-      seg.id = e;
-      seg.n = cnt;
-      seg.base = off;
-      live = true;
-    }
-  }
+  uint64_t members;
+  const bool live = small_down_segment<R>(a, idx, gate_w, seg_i, lds, &seg, &members);
 
   f32x4 acc[1][R][1];
 #pragma unroll
@@ -350,39 +285,7 @@ __global__ __launch_bounds__(1024) void ffn_bf16_down_combine_kernel(FfnArgs a,
           [&](const Stage<1, R, 1, U>& st, int c) { compute_stage(st, acc, lo + c * U, hi); });
     }
   }
-  if (KW > 1) {
-#pragma unroll
-    for (int r = 0; r < R; ++r) red[(wave * R + r) * kWave + lane] = acc[0][r][0];
-  }
-  __syncthreads();
-  if (live && part == 0) {
-    for (int w = 1; w < KW; ++w) {
-#pragma unroll
-      for (int r = 0; r < R; ++r) {
-        const f32x4 p = red[((wave + w) * R + r) * kWave + lane];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) acc[0][r][0][i] += p[i];
-      }
-    }
-    if (rA < seg.n) {
-      const int row = seg.shared ? seg.base + rA : nth_set_bit(members, rA);
-      float* dst = a.out + (size_t)row * a.H;
-#pragma unroll
-      for (int r = 0; r < R; ++r) {
-        *reinterpret_cast<f32x4*>(dst + r0 + 16 * r + 4 * gK) = acc[0][r][0];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) eo_s[row][16 * r + 4 * gK + i] = acc[0][r][0][i];
-      }
-    }
-  }
-  __syncthreads();
-  for (int i = threadIdx.x; i < a.B * kRows; i += blockDim.x) {
-    const int b = i / kRows, c = i - b * kRows;
-    float v = 0.f;
-    for (int j = 0; j < a.k; ++j) v = fmaf(gw_s[b * a.k + j], eo_s[b * a.k + j][c], v);
-    for (int sh = 0; sh < a.S; ++sh) v += eo_s[a.B * a.k + sh * a.B + b][c];
-    y[(size_t)b * a.H + r0 + c] = v;
-  }
+  small_down_finish<R, KW>(a, seg, live, part, members, acc, lds, y, r0);
 }
 
 #ifndef S2MOE_MAX_WAVES
@@ -510,13 +413,10 @@ using TinyLayer = SmallLayer<S2MOE_BF16_TINY>;
 
 }  // namespace
 
-bool moe_layer_small_fits(const FfnArgs& a, float alpha) {
-  return a.wf == kWBf16 && a.B >= 1 && a.B <= kSmallMaxTokens && (alpha == 0.f || a.B == 1) &&
-         TinyLayer::fits(a);
-}
+bool moe_layer_small_fits_bf16(const FfnArgs& a) { return TinyLayer::fits(a); }
 
-hipError_t launch_moe_layer_small(const RouteArgs& ra, const GateArgs& ga, const FfnArgs& a,
-                                  float* y, hipStream_t s) {
+hipError_t launch_moe_layer_small_bf16(const RouteArgs& ra, const GateArgs& ga,
+                                       const FfnArgs& a, float* y, hipStream_t s) {
   return a.packed ? TinyLayer::layer<true>(ra, ga, a, y, s)
                   : TinyLayer::layer<false>(ra, ga, a, y, s);
 }

@@ -47,7 +47,7 @@
 //   the result does not depend on timing.
 #include <atomic>
 
-#include "ffn_common.h"
+#include "small_layer.h"
 
 namespace s2moe {
 
@@ -346,10 +346,11 @@ __device__ __forceinline__ void unit_pass_q(const FfnArgs& a, const Segment& seg
   if (W > 1) __syncthreads();
 }
 
+// The workgroup's unit of the K-split kernel: resolve it from the buckets
+// (global, or LDS in the fused small-batch gate-up) and run its passes.
+// red: W > 1 ? W NM R TMAX x 64 f32x4 of LDS.
 template <int kMode, int TMAX, int R, int W, bool kPacked>
-__global__ __launch_bounds__(W * 64) void ffn_q4_ksplit_kernel(FfnArgs a) {
-  constexpr int NM = kMode == 0 ? 2 : 1;
-  __shared__ f32x4 red[W > 1 ? W * NM * R * TMAX * kWave : 1];
+__device__ __forceinline__ void ffn_q4_ksplit_unit(const FfnArgs& a, f32x4* red) {
   Segment seg;
   int unit;
   if (!resolve_block(a, kMode, 16 * R, &seg, &unit)) return;
@@ -382,6 +383,13 @@ __global__ __launch_bounds__(W * 64) void ffn_q4_ksplit_kernel(FfnArgs a) {
     else
       unit_pass_q<kMode, 1, TMAX, R, W, kPacked>(a, seg, t0, r0, K, C0, C1, S0, S1, red);
   }
+}
+
+template <int kMode, int TMAX, int R, int W, bool kPacked>
+__global__ __launch_bounds__(W * 64) void ffn_q4_ksplit_kernel(FfnArgs a) {
+  constexpr int NM = kMode == 0 ? 2 : 1;
+  __shared__ f32x4 red[W > 1 ? W * NM * R * TMAX * kWave : 1];
+  ffn_q4_ksplit_unit<kMode, TMAX, R, W, kPacked>(a, red);
 }
 
 // Row-split variant (one or two token tiles per pass): the W waves of a
@@ -664,9 +672,9 @@ __global__ __launch_bounds__(256) void q4_reduce_kernel(float* __restrict__ out,
 // x [B, H] bf16 -> x16 [B, H] fp16 in the kernels' order (block_pos, then
 // decode order inside each block), one 8-block per thread (H % 128 == 0, so
 // a row holds whole super-steps).
-__global__ __launch_bounds__(256) void q4_prep_x_kernel(const uint16_t* __restrict__ x,
-                                                        uint16_t* __restrict__ x16, int n8) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+// x (bf16) -> x16 (fp16, the decode order) for 8 elements i of n8.
+__device__ __forceinline__ void prep_x8(const uint16_t* __restrict__ x,
+                                        uint16_t* __restrict__ x16, int i, int n8) {
   if (i >= n8) return;
   const u32x4 v = reinterpret_cast<const u32x4*>(x)[i];
   _Float16 h[8], o[8];
@@ -680,6 +688,107 @@ __global__ __launch_bounds__(256) void q4_prep_x_kernel(const uint16_t* __restri
   u32x4 r;
   __builtin_memcpy(&r, o, 16);
   reinterpret_cast<u32x4*>(x16)[block_pos(i)] = r;
+}
+
+__global__ __launch_bounds__(256) void q4_prep_x_kernel(const uint16_t* __restrict__ x,
+                                                        uint16_t* __restrict__ x16, int n8) {
+  prep_x8(x, x16, blockIdx.x * blockDim.x + threadIdx.x, n8);
+}
+
+// ------------------------------------------------- fused small-batch layer
+// The int4 form of the three-launch small-batch layer (small_layer.h):
+// router rows and the fp16 copy of x in one launch; the K-split gate-up with
+// the routing in its prologue; the down projection with the combine.  Each
+// computes exactly what the unfused launches compute.
+
+// Workgroups [0, gx B) compute the logits (4 per workgroup, as
+// route_rows_kernel), the rest convert x as q4_prep_x_kernel.
+__global__ __launch_bounds__(256) void route_rows_prep_kernel(RouteArgs ra, uint16_t* x16,
+                                                              int n8, int gx) {
+  const int n_route = gx * ra.B;
+  if ((int)blockIdx.x < n_route) {
+    route_row_logit<true>(ra, (blockIdx.x % gx) * 4 + wave_id(), blockIdx.x / gx);
+    return;
+  }
+  prep_x8(static_cast<const uint16_t*>(ra.x), x16, (blockIdx.x - n_route) * 256 + threadIdx.x,
+          n8);
+}
+
+// K-split gate-up with the routing in its prologue (small_layer_routing): the
+// last workgroup publishes the routing and exits; the unit work of the
+// others is ffn_q4_ksplit_kernel<0, 1, R, W>'s, resolved from the LDS
+// buckets.
+template <int NJ, int R, int W, bool kPacked>
+__global__ __launch_bounds__(W * 64) void ffn_q4_gate_up_routed_kernel(FfnArgs a, RouteArgs ra,
+                                                                      GateArgs ga) {
+  __shared__ SmallGateLds rt;
+  __shared__ f32x4 red[W > 1 ? W * 2 * R * kWave : 1];
+  const bool pub = blockIdx.x == gridDim.x - 1;
+  if (wave_id() == 0) small_layer_routing<NJ>(ra, ga, rt, pub);
+  __syncthreads();
+  if (pub) return;
+  ffn_q4_ksplit_unit<0, 1, R, W, kPacked>(with_lds_buckets(a, rt), red);
+}
+
+// Down projection and combine: a workgroup takes 16 R rows of H for every
+// segment (small_down_segment); wave w works on segment w / KW over the
+// super-steps of K part w % KW as the K-split down kernel with KW waves
+// does, and small_down_finish adds the parts in that kernel's order,
+// writes expert_out and forms y.
+template <int R, int KW, bool kPacked>
+__global__ __launch_bounds__(1024) void ffn_q4_down_combine_kernel(FfnArgs a, const int32_t* idx,
+                                                                   const float* gate_w,
+                                                                   float* y) {
+  __shared__ SmallDownLds<R> lds;
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wave = wave_id();
+  const int rA = lane & 15, gK = lane >> 4;
+  const int seg_i = wave / KW, part = wave - seg_i * KW;
+  const int r0 = blockIdx.x * 16 * R;
+  Segment seg;
+  uint64_t members;
+  const bool live = small_down_segment<R>(a, idx, gate_w, seg_i, lds, &seg, &members);
+
+  f32x4 acc[1][R][1];
+#pragma unroll
+  for (int r = 0; r < R; ++r) acc[0][r][0] = f32x4{0.f, 0.f, 0.f, 0.f};
+  if (live) {
+    const int K = seg.shared ? a.Fs : a.F;
+    const int nss = K / 128;
+    const int lo = part * nss / KW, hi = (part + 1) * nss / KW;
+    const size_t mat = (size_t)a.H * K;
+    const uint8_t* C0 = static_cast<const uint8_t*>(seg.shared ? a.sh_down : a.down) +
+                        seg.id * (mat / 2);
+    const uint16_t* S0 = static_cast<const uint16_t*>(seg.shared ? a.sh_down_s : a.down_s) +
+                         seg.id * (mat / 32);
+    const u32x4* xb[1];
+    xb[0] = reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(a.hh) +
+                                           (size_t)x_row(a, 1, seg, min(rA, seg.n - 1)) *
+                                               a.ldh) +
+            gK;
+    const u32x4* pc[R];
+    const uint16_t* ps[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      if (kPacked) {
+        const size_t tile0 = (size_t)(r0 / 16 + r) * nss;
+        pc[r] = reinterpret_cast<const u32x4*>(C0) + tile0 * 64 + lane;
+        ps[r] = S0 + tile0 * 64 + lane;
+      } else {
+        const size_t row = (size_t)(r0 + 16 * r + rA);
+        pc[r] = reinterpret_cast<const u32x4*>(C0 + row * (K / 2)) + gK;
+        ps[r] = S0 + row * (K / 32) + gK;
+      }
+    }
+    if (hi > lo) {
+      const uint32_t magic = opaque(0x64006400u);
+      pipeline2<StageQ<1, R, 1>>(
+          hi - lo,
+          [&](StageQ<1, R, 1>& st, int i) { load_q<kPacked>(st, pc, ps, xb, lo + i); },
+          [&](const StageQ<1, R, 1>& st, int) { compute_q(st, acc, magic); });
+    }
+  }
+  small_down_finish<R, KW>(a, seg, live, part, members, acc, lds, y, r0);
 }
 
 #ifndef S2MOE_Q4_STEPS_PER_WAVE
@@ -802,18 +911,107 @@ hipError_t launch_q4_pair(const FfnArgs& a, hipStream_t s) {
 
 // Tiny batches: the K-split kernel, with the most row tiles per unit (gate-up
 // 2 or 1, down 4, 2 or 1) that still give every compute unit a workgroup.
-hipError_t launch_q4_ksplit(const FfnArgs& a, hipStream_t s) {
+// Row tiles per unit of the K-split launches (launch_q4_ksplit): enough
+// units to give every compute unit one.
+hipError_t ksplit_rows(const FfnArgs& a, int* rg, int* rd) {
   int cus = 0;
-  hipError_t err = device_cus(&cus);
+  const hipError_t err = device_cus(&cus);
   if (err != hipSuccess) return err;
-  err = n_blocks(a, 0, 32) >= cus ? launch_q4_mode<0, 1, 2>(a, s) : launch_q4_mode<0, 1, 1>(a, s);
+  *rg = n_blocks(a, 0, 32) >= cus ? 2 : 1;
+  *rd = n_blocks(a, 1, 64) >= cus ? 4 : (n_blocks(a, 1, 32) >= cus ? 2 : 1);
+  return hipSuccess;
+}
+
+// Waves over K of the K-split down launch with rd row tiles per unit.
+int ksplit_down_waves(const FfnArgs& a, int rd) {
+  int nss = a.F / 128;
+  if (a.S > 0) nss = min(nss, a.Fs / 128);
+  return pick_waves_q4(nss, rd);
+}
+
+hipError_t launch_q4_ksplit(const FfnArgs& a, hipStream_t s) {
+  int rg = 1, rd = 1;
+  hipError_t err = ksplit_rows(a, &rg, &rd);
   if (err != hipSuccess) return err;
-  if (n_blocks(a, 1, 64) >= cus) return launch_q4_mode<1, 1, 4>(a, s);
-  if (n_blocks(a, 1, 32) >= cus) return launch_q4_mode<1, 1, 2>(a, s);
+  err = rg == 2 ? launch_q4_mode<0, 1, 2>(a, s) : launch_q4_mode<0, 1, 1>(a, s);
+  if (err != hipSuccess) return err;
+  if (rd == 4) return launch_q4_mode<1, 1, 4>(a, s);
+  if (rd == 2) return launch_q4_mode<1, 1, 2>(a, s);
   return launch_q4_mode<1, 1, 1>(a, s);
 }
 
+constexpr int kFusedMaxWavesQ4 = 16;
+
+template <int NJ, bool kPacked>
+hipError_t launch_q4_gate_up_routed(const FfnArgs& a, const RouteArgs& ra, const GateArgs& ga,
+                                    int rg, hipStream_t s) {
+  const int w = pick_waves_q4(a.H / 128, 2 * rg);
+  const dim3 grid(n_blocks(a, 0, 16 * rg) + 1);
+  if (rg == 2) {
+    switch (w) {
+      case 1: hipLaunchKernelGGL((ffn_q4_gate_up_routed_kernel<NJ, 2, 1, kPacked>), grid, dim3(64), 0, s, a, ra, ga); break;
+      case 2: hipLaunchKernelGGL((ffn_q4_gate_up_routed_kernel<NJ, 2, 2, kPacked>), grid, dim3(128), 0, s, a, ra, ga); break;
+      case 4: hipLaunchKernelGGL((ffn_q4_gate_up_routed_kernel<NJ, 2, 4, kPacked>), grid, dim3(256), 0, s, a, ra, ga); break;
+      default: hipLaunchKernelGGL((ffn_q4_gate_up_routed_kernel<NJ, 2, 8, kPacked>), grid, dim3(512), 0, s, a, ra, ga); break;
+    }
+  } else {
+    switch (w) {
+      case 1: hipLaunchKernelGGL((ffn_q4_gate_up_routed_kernel<NJ, 1, 1, kPacked>), grid, dim3(64), 0, s, a, ra, ga); break;
+      case 2: hipLaunchKernelGGL((ffn_q4_gate_up_routed_kernel<NJ, 1, 2, kPacked>), grid, dim3(128), 0, s, a, ra, ga); break;
+      case 4: hipLaunchKernelGGL((ffn_q4_gate_up_routed_kernel<NJ, 1, 4, kPacked>), grid, dim3(256), 0, s, a, ra, ga); break;
+      default: hipLaunchKernelGGL((ffn_q4_gate_up_routed_kernel<NJ, 1, 8, kPacked>), grid, dim3(512), 0, s, a, ra, ga); break;
+    }
+  }
+  return hipGetLastError();
+}
+
+template <bool kPacked>
+hipError_t launch_q4_down_combine(const FfnArgs& a, const int32_t* idx, const float* gate_w,
+                                  float* y, int kw, hipStream_t s) {
+  const dim3 grid(a.H / 16);
+  const dim3 block(64 * kw * (a.S + min(a.E, a.B * a.k)));
+  switch (kw) {
+    case 1: hipLaunchKernelGGL((ffn_q4_down_combine_kernel<1, 1, kPacked>), grid, block, 0, s, a, idx, gate_w, y); break;
+    case 2: hipLaunchKernelGGL((ffn_q4_down_combine_kernel<1, 2, kPacked>), grid, block, 0, s, a, idx, gate_w, y); break;
+    case 4: hipLaunchKernelGGL((ffn_q4_down_combine_kernel<1, 4, kPacked>), grid, block, 0, s, a, idx, gate_w, y); break;
+    default: hipLaunchKernelGGL((ffn_q4_down_combine_kernel<1, 8, kPacked>), grid, block, 0, s, a, idx, gate_w, y); break;
+  }
+  return hipGetLastError();
+}
+
+template <bool kPacked>
+hipError_t launch_q4_small_layer(const RouteArgs& ra, const GateArgs& ga, const FfnArgs& a,
+                                 float* y, hipStream_t s) {
+  int rg = 1, rd = 1;
+  hipError_t err = ksplit_rows(a, &rg, &rd);
+  if (err != hipSuccess) return err;
+  const int n8 = a.B * a.H / 8;
+  const int gx = (a.E + 3) / 4;
+  hipLaunchKernelGGL(route_rows_prep_kernel, dim3(gx * a.B + (n8 + 255) / 256), dim3(256), 0, s,
+                     ra, static_cast<uint16_t*>(a.x16), n8, gx);
+  err = hipGetLastError();
+  if (err != hipSuccess) return err;
+  if (a.E <= 64) err = launch_q4_gate_up_routed<1, kPacked>(a, ra, ga, rg, s);
+  else if (a.E <= 128) err = launch_q4_gate_up_routed<2, kPacked>(a, ra, ga, rg, s);
+  else err = launch_q4_gate_up_routed<4, kPacked>(a, ra, ga, rg, s);
+  if (err != hipSuccess) return err;
+  return launch_q4_down_combine<kPacked>(a, ga.idx, ga.gate_w, y, ksplit_down_waves(a, rd), s);
+}
+
 }  // namespace
+
+bool moe_layer_small_fits_q4(const FfnArgs& a) {
+  if (a.B > kQ4KsplitMaxTokens || a.qparts != 1) return false;
+  int rg = 1, rd = 1;
+  if (ksplit_rows(a, &rg, &rd) != hipSuccess) return false;
+  return (a.S + min(a.E, a.B * a.k)) * ksplit_down_waves(a, rd) <= kFusedMaxWavesQ4;
+}
+
+hipError_t launch_moe_layer_small_q4(const RouteArgs& ra, const GateArgs& ga, const FfnArgs& a,
+                                     float* y, hipStream_t s) {
+  return a.packed ? launch_q4_small_layer<true>(ra, ga, a, y, s)
+                  : launch_q4_small_layer<false>(ra, ga, a, y, s);
+}
 
 hipError_t launch_ffn_q4(const FfnArgs& a, hipStream_t s) {
   const int n8 = a.B * a.H / 8;

@@ -193,14 +193,37 @@ hipError_t launch_ffn_bf16(const FfnArgs& a, hipStream_t s);
 hipError_t launch_ffn_q4(const FfnArgs& a, hipStream_t s);
 hipError_t launch_combine(const CombineArgs& a, hipStream_t s);
 
+// Largest batch the single-wave gating takes (B k <= 64 assignments).
+constexpr int kSmallMaxTokens = 4;
+
 // A whole MoE layer of a small batch in three launches (router rows, gate-up
-// with the routing in its prologue, down with the combine; ffn_bf16.hip),
-// the same results bit for bit as launch_route, launch_reuse_gate,
-// launch_ffn and launch_combine in sequence.  moe_layer_small_fits tells
-// whether the layer and batch qualify (bf16 weights, B <= 4 with alpha = 0
-// or B = 1, few enough segments); a carries the same buckets as ga.
-bool moe_layer_small_fits(const FfnArgs& a, float alpha);
-hipError_t launch_moe_layer_small(const RouteArgs& ra, const GateArgs& ga, const FfnArgs& a,
-                                  float* y, hipStream_t s);
+// with the routing in its prologue, down with the combine), the same results
+// bit for bit as launch_route, launch_reuse_gate, launch_ffn and
+// launch_combine in sequence: ffn_bf16.hip for bf16 weights, ffn_q4.hip for
+// int4 (where the first launch also converts x to fp16).  The *_fits
+// functions tell whether the layer's segments fit one workgroup of the down
+// launch; a carries the same buckets as ga.
+bool moe_layer_small_fits_bf16(const FfnArgs& a);
+bool moe_layer_small_fits_q4(const FfnArgs& a);
+hipError_t launch_moe_layer_small_bf16(const RouteArgs& ra, const GateArgs& ga,
+                                       const FfnArgs& a, float* y, hipStream_t s);
+hipError_t launch_moe_layer_small_q4(const RouteArgs& ra, const GateArgs& ga, const FfnArgs& a,
+                                     float* y, hipStream_t s);
+
+// Whether a layer call takes the three-launch path: B <= 4 tokens whose
+// gating keeps the plain top-k (alpha = 0, or one token), bf16 or int4
+// weights, few enough segments.
+inline bool moe_layer_small_fits(const FfnArgs& a, float alpha) {
+  if (a.B < 1 || a.B > kSmallMaxTokens || !(alpha == 0.f || a.B == 1)) return false;
+  if (a.wf == kWBf16) return moe_layer_small_fits_bf16(a);
+  if (a.wf == kWQ4) return moe_layer_small_fits_q4(a);
+  return false;
+}
+
+inline hipError_t launch_moe_layer_small(const RouteArgs& ra, const GateArgs& ga,
+                                         const FfnArgs& a, float* y, hipStream_t s) {
+  return a.wf == kWQ4 ? launch_moe_layer_small_q4(ra, ga, a, y, s)
+                      : launch_moe_layer_small_bf16(ra, ga, a, y, s);
+}
 
 }  // namespace s2moe

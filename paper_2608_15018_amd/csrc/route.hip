@@ -17,21 +17,6 @@ namespace s2moe {
 
 namespace {
 
-// Dot product of one 16-byte chunk of a token row and of a router row.
-template <bool kBf16>
-__device__ __forceinline__ float dot_chunk(u32x4 xc, u32x4 wc, float acc) {
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    if (kBf16) {
-      acc = fmaf(bf16_to_f32(wc[i] & 0xFFFFu), bf16_to_f32(xc[i] & 0xFFFFu), acc);
-      acc = fmaf(bf16_to_f32(wc[i] >> 16), bf16_to_f32(xc[i] >> 16), acc);
-    } else {
-      acc = fmaf(__uint_as_float(wc[i]), __uint_as_float(xc[i]), acc);
-    }
-  }
-  return acc;
-}
-
 // Partial dot products of the token row with 4 router rows (e0 .. e0+3,
 // those < E) over the 16-byte chunks [c_lo, c_hi) of H: lanes split the
 // chunks, so up to 4 iterations x 5 loads are in flight together.
@@ -70,23 +55,10 @@ __host__ __device__ inline int route_slices(int E, int chunks) {
 
 // Small batches and many experts: one wave per (router row, token) pair
 // (grid: E / 4 x B workgroups of 4 waves), so the E rows are streamed by
-// waves spread over the GPU instead of by one workgroup per token.  Lanes
-// take 16-byte chunks of H; a DPP reduction adds them.
+// waves spread over the GPU instead of by one workgroup per token.
 template <bool kBf16>
 __global__ __launch_bounds__(256) void route_rows_kernel(RouteArgs a) {
-  const int lane = threadIdx.x & (kWave - 1);
-  const int e = blockIdx.x * 4 + wave_id();
-  const int b = blockIdx.y;
-  if (e >= a.E) return;
-  const size_t row = (size_t)a.H * (kBf16 ? 2 : 4);
-  const u32x4* wr = reinterpret_cast<const u32x4*>(static_cast<const char*>(a.router) + e * row);
-  const u32x4* xr = reinterpret_cast<const u32x4*>(static_cast<const char*>(a.x) + b * row);
-  const int chunks = a.H / (kBf16 ? 8 : 4);
-  float acc = 0.f;
-#pragma unroll 4
-  for (int c = lane; c < chunks; c += kWave) acc = dot_chunk<kBf16>(xr[c], wr[c], acc);
-  acc = wave_sum_dpp(acc);
-  if (lane == 0) a.logits[(size_t)b * a.E + e] = acc;
+  route_row_logit<kBf16>(a, blockIdx.x * 4 + wave_id(), blockIdx.y);
 }
 
 // Small batches, second launch: one wave per token ranks the logits

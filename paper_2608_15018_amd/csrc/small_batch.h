@@ -13,9 +13,37 @@ namespace s2moe {
 
 constexpr float kLog2e = 1.4426950408889634f;
 
-// Largest batch the one-wave gating takes (B k <= 64 assignments, one per
-// lane).
-constexpr int kSmallMaxTokens = 4;
+// Dot product of one 16-byte chunk of a token row and of a router row.
+template <bool kBf16>
+__device__ __forceinline__ float dot_chunk(u32x4 xc, u32x4 wc, float acc) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    if (kBf16) {
+      acc = fmaf(bf16_to_f32(wc[i] & 0xFFFFu), bf16_to_f32(xc[i] & 0xFFFFu), acc);
+      acc = fmaf(bf16_to_f32(wc[i] >> 16), bf16_to_f32(xc[i] >> 16), acc);
+    } else {
+      acc = fmaf(__uint_as_float(wc[i]), __uint_as_float(xc[i]), acc);
+    }
+  }
+  return acc;
+}
+
+// Logit e of token b by one wave (e >= E: nothing): lanes take 16-byte
+// chunks of H, a DPP reduction adds them, lane 0 writes a.logits[b][e].
+template <bool kBf16>
+__device__ __forceinline__ void route_row_logit(const RouteArgs& a, int e, int b) {
+  const int lane = threadIdx.x & (kWave - 1);
+  if (e >= a.E) return;
+  const size_t row = (size_t)a.H * (kBf16 ? 2 : 4);
+  const u32x4* wr = reinterpret_cast<const u32x4*>(static_cast<const char*>(a.router) + e * row);
+  const u32x4* xr = reinterpret_cast<const u32x4*>(static_cast<const char*>(a.x) + b * row);
+  const int chunks = a.H / (kBf16 ? 8 : 4);
+  float acc = 0.f;
+#pragma unroll 4
+  for (int c = lane; c < chunks; c += kWave) acc = dot_chunk<kBf16>(xr[c], wr[c], acc);
+  acc = wave_sum_dpp(acc);
+  if (lane == 0) a.logits[(size_t)b * a.E + e] = acc;
+}
 
 // Orders the LDS and global accesses of one wave before and after it (the
 // functions below run on a single wave, also inside larger workgroups whose

@@ -3,12 +3,13 @@
 * Bit for bit equal to s2moe_route, s2moe_reuse_gate, s2moe_verify_moe and
   s2moe_combine called in turn, in every routing array, expert_out and y:
   on batches that take the three-launch path (B <= 4 with alpha = 0, or one
-  token; bf16 weights; E of 8 to 200, so one, two or four experts per lane
-  in the ranking; shared experts; down K split over 1 and 4 waves; packed
-  and row-major weights) and on batches that do not (alpha > 0 at B = 2,
-  too many segments, B = 8, int4 and fp32 weights).
+  token; bf16 and int4 weights; E of 8 to 200, so one, two or four experts
+  per lane in the ranking; shared experts; down K split over 1 and 4 waves;
+  packed and row-major weights) and on batches that do not (alpha > 0 at
+  B = 2, too many segments, B = 8, B = 16, fp32 weights).
 * The number of launches, read from a captured HIP graph: 3 on the fused
-  path against 6 for the same layer as four calls; one fewer than the four
+  path against 6 (bf16) or 7 (int4: x to fp16 is a launch of its own) for
+  the same layer as four calls; one fewer than the four
   calls where the gating launch ranks the logits itself; the same count
   where the routing ranks in its own workgroups or the logits are too many
   to stage.
@@ -60,9 +61,16 @@ CASES = [
     ("k16 B4 (four calls)", _shape(n_experts=64, top_k=16, cap=16), 4, False),
     ("F2048 B2 (four calls)", _shape(ffn=2048, n_experts=16, top_k=3, cap=3), 2, False),
     ("B8 (four calls)", _shape(), 8, False),
-    ("int4 B2 (four calls)", _shape(wdt="q4g32"), 2, False),
+    ("int4 B2", _shape(wdt="q4g32"), 2, True),
     ("fp32 B1 (four calls)", _shape(act="f32", wdt="f32"), 1, False),
     ("B16 E8 (route_kernel)", _shape(cap=4, alpha=0.5), 16, False),
+    ("int4 e64 k3 B4 shared", _shape(hidden=512, ffn=256, n_experts=64, top_k=3, cap=3,
+                                     n_shared=2, ffn_shared=256, wdt="q4g32"), 4, True),
+    ("int4 e128 k3 B1 F1024", _shape(hidden=512, ffn=1024, n_experts=128, top_k=3, cap=3,
+                                     wdt="q4g32"), 1, True),
+    ("int4 alpha B1", _shape(n_experts=32, top_k=4, cap=8, alpha=0.7, wdt="q4g32"), 1, True),
+    ("int4 alpha B2 (four calls)", _shape(n_experts=32, top_k=4, cap=8, alpha=0.7,
+                                          wdt="q4g32"), 2, False),
     ("B64 E256 (unstaged gate)", _shape(ffn=256, n_experts=256, top_k=4, cap=8, alpha=0.5), 64,
      False),
 ]
@@ -131,7 +139,13 @@ def test_moe_layer_equals_four_calls(label, shape, B, fused, packed):
     got1, got4 = p1.results(), p4.results()
     _assert_same(got1, got4, tag)
     if fused:
-        ref = oracle.forward(d["x"], d["router"], d["conf_w"], d["experts"], d["shared"], shape)
+        ex, sh, sref = d["experts"], d["shared"], shape
+        if shape.wdt == "q4g32":
+            deq = lambda e: {n: np.stack([oracle.dequant_q4g32(e[n][i], e[n + "_s"][i])  # noqa: E731
+                                          for i in range(e[n].shape[0])]).astype(np.float32)
+                             for n in ("gate", "up", "down")} if e else {}
+            ex, sh, sref = deq(ex), deq(sh), shape.with_(wdt="f32")
+        ref = oracle.forward(d["x"], d["router"], d["conf_w"], ex, sh, sref)
         check_routing(got1, ref, tag)
         check_outputs(got1, ref, shape.wdt, tag)
     log(f"[moe_layer] {tag}: equal, n_uniq={got1['n_uniq']}")
@@ -141,7 +155,8 @@ def test_moe_layer_equals_four_calls(label, shape, B, fused, packed):
 # fused path; elsewhere the gating launch ranks the logits itself where the
 # routing would rank them in a launch of its own (B <= 8 or E > 64, logits
 # staged in LDS or a single-wave gate), and nothing changes otherwise.
-LAUNCHES = [(1, 3, 6), (2, 3, 6), (8, 5, 6), (12, 6, 7), (14, 5, 5), (15, 6, 6)]
+LAUNCHES = [(1, 3, 6), (2, 3, 6), (8, 5, 6), (12, 3, 7), (14, 5, 5), (19, 6, 6), (15, 3, 7),
+            (18, 6, 7)]
 
 
 @pytest.mark.parametrize("case,n_call,n_four", LAUNCHES, ids=[CASES[c[0]][0] for c in LAUNCHES])
