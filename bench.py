@@ -637,7 +637,9 @@ def bench_layer(args, wl, shape, B: int, default_B: int, wid: int, stream_ref: b
         shape.n_shared * expert_bytes(shape, shape.ffn_shared)
 
     # Timed region 1: K whole steps back to back (no host sync, no events),
-    # each one s2moe_moe_layer call; then the same steps as the four calls.
+    # each one s2moe_moe_layer call.  The same steps as the four calls are
+    # timed in blocks of K alternating with blocks of one-call steps, so
+    # that the two compare under the same conditions.
     torch.cuda.synchronize()
     t_start = time.perf_counter()
     for _ in range(args.steps):
@@ -647,11 +649,16 @@ def bench_layer(args, wl, shape, B: int, default_B: int, wid: int, stream_ref: b
     ms_per_step = elapsed / args.steps * 1e3
     p4(xd, rd, cd, wstruct)
     torch.cuda.synchronize()
-    t4 = time.perf_counter()
-    for _ in range(args.steps):
-        p4(xd, rd, cd, wstruct)
-    torch.cuda.synchronize()
-    four_call_ms = (time.perf_counter() - t4) / args.steps * 1e3
+    cmp = {p: 0.0, p4: 0.0}
+    for _ in range(2):
+        for q in (p4, p):
+            tq = time.perf_counter()
+            for _ in range(args.steps):
+                q(xd, rd, cd, wstruct)
+            torch.cuda.synchronize()
+            cmp[q] += time.perf_counter() - tq
+    four_call_ms = cmp[p4] / (2 * args.steps) * 1e3
+    one_call_cmp_ms = cmp[p] / (2 * args.steps) * 1e3
 
     # Timed region 2: K back-to-back s2moe_verify_moe calls between one pair
     # of HIP events on the launch stream (an event pair costs a few
@@ -730,6 +737,7 @@ def bench_layer(args, wl, shape, B: int, default_B: int, wid: int, stream_ref: b
         "ffn_timing": ffn_note,
         "step": "one s2moe_moe_layer call (route, gate, experts, combine)",
         "four_call_ms_per_step": four_call_ms,
+        "one_call_ms_per_step_alternating": one_call_cmp_ms,
     }
     if stream_gbs is not None:
         out["stream_read"] = {"value": stream_gbs, "unit": "GB/s",

@@ -292,11 +292,17 @@ __global__ __launch_bounds__(1024) void ffn_bf16_down_combine_kernel(FfnArgs a,
 #define S2MOE_MAX_WAVES 8
 #endif
 
+#ifndef S2MOE_MAX_RED_TILES
+#define S2MOE_MAX_RED_TILES 32
+#endif
+
 // Waves per unit: enough that each streams >= spw K steps, a power of two,
-// and the reduction buffer stays within 32 KB of LDS.
+// and the reduction buffer stays within S2MOE_MAX_RED_TILES KB of LDS.
 int pick_waves(int nks, int tiles, int spw) {
   int w = 1;
-  while (w * 2 <= S2MOE_MAX_WAVES && nks / (w * 2) >= spw && (w * 2) * tiles <= 32) w *= 2;
+  while (w * 2 <= S2MOE_MAX_WAVES && nks / (w * 2) >= spw &&
+         (w * 2) * tiles <= S2MOE_MAX_RED_TILES)
+    w *= 2;
   return w;
 }
 
