@@ -161,6 +161,26 @@ def recorded_traffic(name: str, wdt: str, B: int, default_B: int):
     return None
 
 
+# Warm-up lasts at least this long: the shader clock settles under load
+# over a few hundred microseconds to milliseconds, and the int4 kernels,
+# bound by instruction issue, follow it.
+WARMUP_MIN_S = 0.2
+
+
+def warm(fn, steps: int):
+    """Run fn() at least max(1, steps) times and until WARMUP_MIN_S of GPU
+    time has passed (untimed)."""
+    import torch
+    n, t0 = 0, time.perf_counter()
+    while n < max(1, steps) or time.perf_counter() - t0 < WARMUP_MIN_S:
+        fn()
+        n += 1
+        if n % 8 == 0:
+            torch.cuda.synchronize()
+    torch.cuda.synchronize()
+    return n
+
+
 def _head_start():
     """Queue a short GPU spin so that the host enqueues the timed launches
     while the GPU is still busy: the events then bracket kernels that run
@@ -201,9 +221,7 @@ def bench_expand(args) -> int:
         s2.expand(dd["parent"], dd["q"], dd["eid"], dd["c_draft"], dd["n_nodes"], o,
                   wl.n_experts, wl.t_ar, wl.t_exp, root_eid=dd["root_eid"])
 
-    for _ in range(max(1, args.warmup)):
-        launch()
-    torch.cuda.synchronize()
+    warm(launch, args.warmup)
     res = out.host()
 
     # Timed: K back-to-back launches between one pair of HIP events on the
@@ -325,9 +343,7 @@ def bench_draft(args) -> int:
     torch.cuda.synchronize()
     _log(f"[bench] draft {name}: {n_sets} weight sets, {L} layers in {time.time() - t0:.1f}s")
     step = draft.DraftStep(layer, B, inputs)
-    for _ in range(max(1, args.warmup)):
-        step()
-    torch.cuda.synchronize()
+    warm(step, args.warmup)
     n_uniq = [int(p.rt.n_uniq.item()) for p in step.passes]
     e_bytes = expert_bytes(layer_shape_of(m, wdt), F)
     s_bytes = expert_bytes(layer_shape_of(m, wdt), Fs) if S else 0
@@ -468,9 +484,7 @@ def bench_stack(args, wl, shape, B: int, wid: int) -> int:
         for p, (x, r, c, w) in zip(passes, ins):
             p(x, r, c, w)
 
-    for _ in range(max(1, args.warmup)):
-        step()
-    torch.cuda.synchronize()
+    warm(step, args.warmup)
     n_uniq = [int(p.rt.n_uniq.item()) for p in passes]
     nbytes = sum(n_uniq) * expert_bytes(shape, F) + L * S * expert_bytes(shape, Fs)
 
@@ -629,9 +643,7 @@ def bench_layer(args, wl, shape, B: int, default_B: int, wid: int, stream_ref: b
     stream = torch.cuda.current_stream()
 
     # warm-up (also fixes the routing, which is deterministic)
-    for _ in range(max(1, args.warmup)):
-        p(xd, rd, cd, wstruct)
-    torch.cuda.synchronize()
+    warmup_run = warm(lambda: p(xd, rd, cd, wstruct), args.warmup)
     n_uniq = int(p.rt.n_uniq.item())
     unique_bytes = n_uniq * expert_bytes(shape, shape.ffn) + \
         shape.n_shared * expert_bytes(shape, shape.ffn_shared)
@@ -736,6 +748,7 @@ def bench_layer(args, wl, shape, B: int, default_B: int, wid: int, stream_ref: b
         "reuse_ratio": n_uniq / (B * shape.top_k),
         "ffn_timing": ffn_note,
         "step": "one s2moe_moe_layer call (route, gate, experts, combine)",
+        "warmup_steps_run": warmup_run,
         "four_call_ms_per_step": four_call_ms,
         "one_call_ms_per_step_alternating": one_call_cmp_ms,
     }
