@@ -103,11 +103,13 @@ def random_batch(rng, T, N, L, E, k, ragged=True, dup_ids=True, bad=0.0):
     (5, 1, 1, 1, 1), (6, 33, 3, 7, 2), (4, 97, 5, 40, 3), (3, 256, 4, 64, 4),
     (3, 257, 4, 32, 2), (2, 511, 2, 33, 5), (2, 700, 2, 16, 3), (2, 1024, 2, 8, 2),
     (3, 64, 7, 1024, 1), (2, 16, 128, 8, 32),
+    (3, 200, 6, 128, 5), (2, 300, 3, 255, 3), (2, 64, 9, 250, 7), (3, 120, 48, 128, 8),
 ])
 def test_random_trees_across_tilings(T, N, L, E, k):
     """Random tree shapes (any earlier node as parent), padding and repeated
     ids, ragged node counts including 0 and N; N spans 1, 2 and 4 nodes per
-    thread and E spans 1..1024."""
+    thread and E spans 1..1024 (k 5-8 at E 128-255 too, ids unaligned with
+    16-byte chunks when L k is odd)."""
     rng = np.random.default_rng(T * 1000 + N)
     a = random_batch(rng, T, N, L, E, k)
     t_exp = 0.5 / max(1, L * k)
