@@ -14,8 +14,8 @@ Timing: per configuration, `steps` back-to-back passes between one pair of
 HIP events on the launch stream, cycling through copies of the expert
 weights large enough that the last-level cache cannot serve a pass from the
 previous one (the protocol of bench.py); the average is used.  Two
-latencies are fitted: the whole pass (route -> gate -> experts -> combine)
-and the expert-FFN call alone.
+latencies are fitted: the whole pass (one s2moe_moe_layer call: route ->
+gate -> experts -> combine) and the expert-FFN call alone.
 """
 
 from __future__ import annotations
@@ -118,7 +118,7 @@ def measure(workload: str, batches, alphas, seeds, steps: int = 20, device="cuda
                 rd, xd, cd = (to_device(a, device) for a in (router, x, conf_w))
                 layer = _lib.make_layer(shape, flags=shape.flags | (
                     _lib.PACKED_WEIGHTS if packed else 0))
-                p = VerifyPass(layer, B, device)
+                p = VerifyPass(layer, B, device, fused=True)
                 p(xd, rd, cd, wstruct)
                 torch.cuda.synchronize()
                 n_uniq = int(p.rt.n_uniq.item())
