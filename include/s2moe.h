@@ -228,14 +228,17 @@ s2moe_status s2moe_combine(const s2moe_layer *layer, int32_t n_tokens,
    in that order, with the same results bit for bit in every output (r's
    arrays, expert_out, y) and the same argument checks and errors.
    A batch whose gating cannot move the plain top-k (alpha = 0, or
-   n_tokens = 1) and that has at most 4 tokens, BF16 weights and at most 16
-   waves' worth of segments (S + min(E, B k) segments, each taking as many
-   waves as the down launch splits its K into) runs as three launches
-   instead of six: the router rows; the gate-up projection, where every
-   workgroup first ranks the logits and buckets the batch itself; and the
-   down projection with the combine folded in.  Every other batch runs the
-   four calls' kernels one after another.  Layer dispatch cost dominates
-   such small batches (a draft step runs one per MoE layer and token).
+   n_tokens = 1) and that has at most 4 tokens, BF16 or Q4G32 weights and at
+   most 16 waves' worth of segments (S + min(E, B k) segments, each taking
+   as many waves as the down launch splits its K into) runs as three
+   launches instead of six (seven for Q4G32): the router rows (with Q4G32
+   also the fp16 copy of x); the gate-up projection, where every workgroup
+   first ranks the logits and buckets the batch itself; and the down
+   projection with the combine folded in.  Every other batch runs the four
+   calls' kernels one after another, except that the gating launch ranks
+   the logits itself where the routing would rank them in a launch of its
+   own.  Layer dispatch cost dominates such small batches (a draft step
+   runs one per MoE layer and token).
    Workspace, ownership and stream as for s2moe_verify_moe; y as for
    s2moe_combine. */
 s2moe_status s2moe_moe_layer(const s2moe_layer *layer, int32_t n_tokens, const void *x,
