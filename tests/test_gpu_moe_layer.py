@@ -197,3 +197,39 @@ def test_moe_layer_graph_replays():
         p(*ins, w)
         torch.cuda.synchronize()
     log("[moe_layer] graph replays equal the eager call")
+
+
+def _random_case(rng):
+    """A random layer and batch inside the ABI limits, small enough for the
+    host generator: both sides of the three-launch boundary."""
+    wdt = rng.choice(["bf16", "bf16", "q4g32", "f32"])
+    mult = 128 if wdt == "q4g32" else 64
+    E = int(rng.choice([4, 8, 16, 33, 64, 100, 128, 200]))
+    k = int(rng.integers(1, min(E - 1, 16) + 1))
+    cap = int(rng.integers(k, min(E, 3 * k) + 1))
+    S = int(rng.choice([0, 0, 1, 2]))
+    shape = LayerShape(hidden=mult * int(rng.integers(1, 5)), ffn=mult * int(rng.integers(1, 9)),
+                       n_experts=E, top_k=k, cap=cap, alpha=float(rng.choice([0.0, 0.0, 0.6])),
+                       n_shared=S, ffn_shared=mult * int(rng.integers(1, 5)) if S else 0,
+                       flags=int(rng.choice([0, 0, 1, 4, 7])),
+                       act="f32" if wdt == "f32" else "bf16", wdt=wdt)
+    B = int(rng.choice([1, 1, 2, 3, 4, 4, 5, 8, 12]))
+    return shape, B
+
+
+@pytest.mark.parametrize("seed", range(24))
+def test_moe_layer_random_shapes(seed):
+    """Random layers (E 4-200, k 1-16, shared experts, fp32/bf16/int4,
+    flags, alpha 0 or 0.6, B 1-12): one call equals the four calls bit for
+    bit in every output."""
+    rng = np.random.default_rng(1000 + seed)
+    shape, B = _random_case(rng)
+    d = make_inputs(shape, B, seed=seed, rho=0.5)
+    packed = shape.wdt != "f32" and bool(seed % 2)
+    tag = (f"random {seed}: H={shape.hidden} F={shape.ffn} E={shape.n_experts} k={shape.top_k} "
+           f"cap={shape.cap} S={shape.n_shared} B={B} a={shape.alpha} flags={shape.flags} "
+           f"{shape.wdt} packed={packed}")
+    log(f"[moe_layer] {tag}")
+    p1, _, _, _d1 = _run(shape, d, fused=True, packed=packed)
+    p4, _, _, _d4 = _run(shape, d, fused=False, packed=packed)
+    _assert_same(p1.results(), p4.results(), tag)
