@@ -250,7 +250,7 @@ def verify_moe_noalloc(layer: Layer, x: torch.Tensor, weights: Weights, rt: Rout
                                            _ptr(expert_out), _stream(stream)))
 
 
-NOALLOC_SCRATCH_BYTES = 8 << 20
+NOALLOC_SCRATCH_BYTES = 16 << 20
 
 
 def combine(layer: Layer, rt: Routing, expert_out: torch.Tensor, y: torch.Tensor, stream=None):

@@ -33,8 +33,8 @@ def _compile(src: str, objdir: str = OBJDIR, defines=()) -> str:
     out = os.path.join(objdir, os.path.splitext(src)[0] + ".o")
     cmd = [HIPCC, *COMMON, *DEVICE_FLAGS, *defines, "-c", os.path.join(CSRC, src), "-o", out]
     if src.endswith(".cpp"):
-        cmd = [HIPCC, *COMMON, "-x", "c++", "-D__HIP_PLATFORM_AMD__=1", "-I", ROCM_INC, "-c",
-               os.path.join(CSRC, src), "-o", out]
+        cmd = [HIPCC, *COMMON, "-x", "c++", "-D__HIP_PLATFORM_AMD__=1", "-I", ROCM_INC, *defines,
+               "-c", os.path.join(CSRC, src), "-o", out]
     r = subprocess.run(cmd, capture_output=True, text=True)
     noise = "is not a recognized feature for this target"
     msg = "\n".join(l for l in (r.stdout + r.stderr).splitlines() if noise not in l)

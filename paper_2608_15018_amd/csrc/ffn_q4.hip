@@ -895,9 +895,6 @@ hipError_t launch_q4_layout(const FfnArgs& a, int Q, hipStream_t s) {
 #ifndef S2MOE_Q4_GATEUP_R
 #define S2MOE_Q4_GATEUP_R 1
 #endif
-#ifndef S2MOE_Q4_DOWN_R
-#define S2MOE_Q4_DOWN_R 2
-#endif
 
 template <int TMAX>
 hipError_t launch_q4_pair(const FfnArgs& a, hipStream_t s) {

@@ -227,7 +227,7 @@ def test_combine_rejects_overlapping_output(lib):
 def test_noalloc_verify_rejects_oversized_scratch_on_host(lib):
     """A layer whose workspace exceeds the library's scratch array is
     rejected before anything touches the device (no GPU needed)."""
-    L = _layer(hidden=4096, ffn=14336, n_experts=8, top_k=2, cap=4)
+    L = _layer(hidden=4096, ffn=32768, n_experts=8, top_k=2, cap=4)
     w = _lib.Weights(*([0x300000] * 12))
     rt = _lib.RoutingStruct(*([0x200000] * 12))
     fake = ctypes.c_void_p(0x100000)
