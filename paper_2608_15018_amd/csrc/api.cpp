@@ -166,6 +166,8 @@ s2moe_status route_args(const char* fn, const s2moe_layer* layer, int32_t n_toke
   a.E = layer->n_experts;
   a.k = layer->top_k;
   a.bf16 = layer->act_dtype == S2MOE_BF16;
+  a.x16 = nullptr;
+  a.n8 = 0;
   return S2MOE_OK;
 }
 
@@ -366,6 +368,8 @@ s2moe_status verify_args(const char* fn, const s2moe_layer* layer, int32_t n_tok
   a.x16 = nullptr;
   a.part = nullptr;
   a.qparts = q4 ? q4_parts(layer, n_tokens) : 1;
+  a.x16_ready = false;
+  a.defer_reduce = false;
   a.out = expert_out;
   a.packed = (layer->flags & S2MOE_PACKED_WEIGHTS) != 0;
   return S2MOE_OK;
@@ -614,9 +618,19 @@ s2moe_status s2moe_moe_layer(const s2moe_layer* layer, int32_t n_tokens, const v
   const hipStream_t s = static_cast<hipStream_t>(stream);
   if (s2moe::moe_layer_small_fits(fa, layer->alpha))
     return hip_status(fn, s2moe::launch_moe_layer_small(ra, ga, fa, y, s));
+  if (fa.wf == s2moe::kWQ4) {
+    // The routing launch also writes the fp16 copy of x, and the combine
+    // launch also adds the down projection's K parts.
+    ra.x16 = static_cast<uint16_t*>(fa.x16);
+    ra.n8 = n_tokens * layer->hidden / 8;
+    fa.x16_ready = true;
+    fa.defer_reduce = fa.qparts > 1;
+  }
   hipError_t err = s2moe::launch_route_and_gate(ra, ga, s);
   if (err == hipSuccess) err = s2moe::launch_ffn(fa, s);
-  if (err == hipSuccess) err = s2moe::launch_combine(ca, s);
+  if (err == hipSuccess)
+    err = fa.defer_reduce ? s2moe::launch_q4_reduce_combine(fa, ca, s)
+                          : s2moe::launch_combine(ca, s);
   return hip_status(fn, err);
 }
 

@@ -47,6 +47,7 @@
 //   the result does not depend on timing.
 #include <atomic>
 
+#include "q4_layout.h"
 #include "small_layer.h"
 
 namespace s2moe {
@@ -72,18 +73,6 @@ __device__ __forceinline__ half8v as_half8(u32x4 v) {
   half8v r;
   __builtin_memcpy(&r, &v, 16);
   return r;
-}
-
-// Position of element e of an 8-element block in the decode order
-// (0,4,1,5,2,6,3,7).
-__device__ __forceinline__ int pos8(int e) { return ((e & 3) << 1) | (e >> 2); }
-
-// Where 8-block c of a row of activations is stored: inside each 128-wide
-// super-step (16 blocks, block 4 g + j = dword j of code group g) the blocks
-// are stored j-major, so that the four lanes of one token that feed MFMA j
-// read 64 contiguous bytes.
-__host__ __device__ __forceinline__ int block_pos(int c) {
-  return (c & ~15) | ((c & 3) << 2) | ((c >> 2) & 3);
 }
 
 // The value unchanged but held in a register the compiler cannot see through,
@@ -669,27 +658,46 @@ __global__ __launch_bounds__(256) void q4_reduce_kernel(float* __restrict__ out,
   reinterpret_cast<f32x4*>(out)[i] = v;
 }
 
-// x [B, H] bf16 -> x16 [B, H] fp16 in the kernels' order (block_pos, then
-// decode order inside each block), one 8-block per thread (H % 128 == 0, so
-// a row holds whole super-steps).
-// x (bf16) -> x16 (fp16, the decode order) for 8 elements i of n8.
-__device__ __forceinline__ void prep_x8(const uint16_t* __restrict__ x,
-                                        uint16_t* __restrict__ x16, int i, int n8) {
-  if (i >= n8) return;
-  const u32x4 v = reinterpret_cast<const u32x4*>(x)[i];
-  _Float16 h[8], o[8];
+// The ordered reduce and the combine in one launch (the one-call layer): for
+// token b and 4 columns, each of its output rows (the k routed rows b k + j,
+// then the shared rows B k + s B + b) gets parts 1 .. Q - 1 added in part
+// order and goes back to expert_out, as q4_reduce_kernel does; y is then
+// formed from those rows with combine_kernel's arithmetic.
+__global__ __launch_bounds__(256) void q4_reduce_combine_kernel(FfnArgs a, CombineArgs c) {
+  const int b = blockIdx.y;
+  const int col = blockIdx.x * blockDim.x + threadIdx.x;
+  if (col * 4 >= a.H) return;
+  const int ldq = a.H / 4;
+  const size_t n4 = ((size_t)a.B * a.k + (size_t)a.S * a.B) * ldq;
+  f32x4* out = reinterpret_cast<f32x4*>(a.out);
+  const f32x4* part = reinterpret_cast<const f32x4*>(a.part);
+  auto reduce_row = [&](int r) {
+    const size_t i = (size_t)r * ldq + col;
+    f32x4 v = out[i];
+    for (int q = 1; q < a.qparts; ++q) {
+      const f32x4 p = part[(size_t)(q - 1) * n4 + i];
 #pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    h[2 * q] = (_Float16)bf16_to_f32(v[q] & 0xFFFFu);
-    h[2 * q + 1] = (_Float16)bf16_to_f32(v[q] >> 16);
+      for (int e = 0; e < 4; ++e) v[e] += p[e];
+    }
+    out[i] = v;
+    return v;
+  };
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  for (int j = 0; j < a.k; ++j) {
+    const float w = c.gate_w[b * a.k + j];
+    const f32x4 v = reduce_row(b * a.k + j);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) acc[e] = fmaf(w, v[e], acc[e]);
   }
+  for (int sh = 0; sh < a.S; ++sh) {
+    const f32x4 v = reduce_row(a.B * a.k + sh * a.B + b);
 #pragma unroll
-  for (int e = 0; e < 8; ++e) o[pos8(e)] = h[e];
-  u32x4 r;
-  __builtin_memcpy(&r, o, 16);
-  reinterpret_cast<u32x4*>(x16)[block_pos(i)] = r;
+    for (int e = 0; e < 4; ++e) acc[e] += v[e];
+  }
+  reinterpret_cast<f32x4*>(c.y)[(size_t)b * ldq + col] = acc;
 }
 
+// x [B, H] bf16 -> x16 [B, H] fp16 in the kernels' order (prep_x8).
 __global__ __launch_bounds__(256) void q4_prep_x_kernel(const uint16_t* __restrict__ x,
                                                         uint16_t* __restrict__ x16, int n8) {
   prep_x8(x, x16, blockIdx.x * blockDim.x + threadIdx.x, n8);
@@ -1010,18 +1018,27 @@ hipError_t launch_moe_layer_small_q4(const RouteArgs& ra, const GateArgs& ga, co
                   : launch_q4_small_layer<false>(ra, ga, a, y, s);
 }
 
+hipError_t launch_q4_reduce_combine(const FfnArgs& a, const CombineArgs& c, hipStream_t s) {
+  hipLaunchKernelGGL(q4_reduce_combine_kernel, dim3((a.H / 4 + 255) / 256, a.B), dim3(256), 0, s,
+                     a, c);
+  return hipGetLastError();
+}
+
 hipError_t launch_ffn_q4(const FfnArgs& a, hipStream_t s) {
-  const int n8 = a.B * a.H / 8;
-  hipLaunchKernelGGL(q4_prep_x_kernel, dim3((n8 + 255) / 256), dim3(256), 0, s,
-                     static_cast<const uint16_t*>(a.x), static_cast<uint16_t*>(a.x16), n8);
-  hipError_t err = hipGetLastError();
-  if (err != hipSuccess) return err;
+  hipError_t err = hipSuccess;
+  if (!a.x16_ready) {
+    const int n8 = a.B * a.H / 8;
+    hipLaunchKernelGGL(q4_prep_x_kernel, dim3((n8 + 255) / 256), dim3(256), 0, s,
+                       static_cast<const uint16_t*>(a.x), static_cast<uint16_t*>(a.x16), n8);
+    err = hipGetLastError();
+    if (err != hipSuccess) return err;
+  }
   if (a.B <= kQ4KsplitMaxTokens) return launch_q4_ksplit(a, s);
   // Token tiles held in one pass: the batch bounds every bucket.
   if (a.B <= 16) err = launch_q4_pair<1>(a, s);
   else if (a.B <= 32) err = launch_q4_pair<2>(a, s);
   else err = launch_q4_pair<S2MOE_Q4_TMAX_LARGE>(a, s);
-  if (err != hipSuccess || a.qparts <= 1) return err;
+  if (err != hipSuccess || a.qparts <= 1 || a.defer_reduce) return err;
   const size_t n4 = ((size_t)a.B * a.k + (size_t)a.S * a.B) * a.H / 4;
   hipLaunchKernelGGL(q4_reduce_kernel, dim3((unsigned)((n4 + 255) / 256)), dim3(256), 0, s, a.out,
                      a.part, a.qparts, n4);

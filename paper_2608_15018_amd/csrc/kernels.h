@@ -27,6 +27,11 @@ struct RouteArgs {
   float* gap;
   int B, H, E, k;
   bool bf16;
+  // When set (bf16 x, one-call layer with int4 weights): the routing launch
+  // also converts x to the int4 path's fp16 copy, n8 8-blocks, in
+  // workgroups of its own.
+  uint16_t* x16;
+  int n8;
 };
 
 struct GateArgs {
@@ -71,6 +76,8 @@ struct FfnArgs {
   float* part;  // workspace, int4 weights only: down partial sums of K parts 1..Q-1,
                 // [Q - 1][B*k + S*B][H] fp32 (unused when Q == 1)
   int qparts;   // Q: K parts of the int4 down projection (q4_down_parts)
+  bool x16_ready;     // int4: x16 already written (by the routing launch)
+  bool defer_reduce;  // int4: leave the K parts' reduce to launch_q4_reduce_combine
   bool packed;  // weights in the packed tile order (pack.hip)
   float* out;  // [B*k + S*B, H]
 };
@@ -204,6 +211,10 @@ hipError_t launch_ffn(const FfnArgs& a, hipStream_t s);
 hipError_t launch_ffn_bf16(const FfnArgs& a, hipStream_t s);
 hipError_t launch_ffn_q4(const FfnArgs& a, hipStream_t s);
 hipError_t launch_combine(const CombineArgs& a, hipStream_t s);
+// int4 weights with K parts and defer_reduce: the parts' ordered reduce into
+// expert_out and the combine in one launch, the same results bit for bit as
+// the reduce in launch_ffn then launch_combine (ffn_q4.hip).
+hipError_t launch_q4_reduce_combine(const FfnArgs& a, const CombineArgs& c, hipStream_t s);
 
 // Largest batch the single-wave gating takes (B k <= 64 assignments).
 constexpr int kSmallMaxTokens = 4;

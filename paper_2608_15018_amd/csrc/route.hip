@@ -11,6 +11,7 @@
 // reductions add the lane partials and the slices are summed in order.
 // Wave 0 then ranks the E logits: an exact top-(k+1) by ballots over the
 // order keys, as in the gating kernel.
+#include "q4_layout.h"
 #include "small_batch.h"
 
 namespace s2moe {
@@ -58,6 +59,12 @@ __host__ __device__ inline int route_slices(int E, int chunks) {
 // waves spread over the GPU instead of by one workgroup per token.
 template <bool kBf16>
 __global__ __launch_bounds__(256) void route_rows_kernel(RouteArgs a) {
+  if ((int)blockIdx.y >= a.B) {
+    // Rows of workgroups past the B tokens convert x (a.x16 set).
+    const int blk = (blockIdx.y - a.B) * gridDim.x + blockIdx.x;
+    prep_x8(static_cast<const uint16_t*>(a.x), a.x16, blk * 256 + threadIdx.x, a.n8);
+    return;
+  }
   route_row_logit<kBf16>(a, blockIdx.x * 4 + wave_id(), blockIdx.y);
 }
 
@@ -72,6 +79,12 @@ __global__ __launch_bounds__(kWave) void route_select_wave_kernel(RouteArgs a) {
 
 template <bool kBf16, int NJ>
 __global__ __launch_bounds__(1024) void route_kernel(RouteArgs a) {
+  if ((int)blockIdx.x >= a.B) {
+    // Workgroups past the B tokens convert x (a.x16 set).
+    prep_x8(static_cast<const uint16_t*>(a.x), a.x16,
+            (blockIdx.x - a.B) * blockDim.x + threadIdx.x, a.n8);
+    return;
+  }
   __shared__ float part_s[kMaxExperts];  // [slice][E]: slices * E <= 256
   __shared__ float ell_s[kMaxExperts];
   const int tid = threadIdx.x;
@@ -127,7 +140,9 @@ __global__ __launch_bounds__(1024) void route_kernel(RouteArgs a) {
 #endif
 
 hipError_t launch_route_rows(const RouteArgs& a, hipStream_t s) {
-  const dim3 grid((a.E + 3) / 4, a.B);
+  const int gx = (a.E + 3) / 4;
+  const int prep_rows = a.x16 ? (a.n8 + 256 * gx - 1) / (256 * gx) : 0;
+  const dim3 grid(gx, a.B + prep_rows);
   if (a.bf16)
     hipLaunchKernelGGL(route_rows_kernel<true>, grid, dim3(256), 0, s, a);
   else
@@ -156,15 +171,16 @@ hipError_t launch_route(const RouteArgs& a, hipStream_t s) {
   const int chunks = a.H / (a.bf16 ? 8 : 4);
   const int waves = min(16, route_slices(a.E, chunks) * ((a.E + 3) / 4));
   const dim3 block(64 * waves);
+  const dim3 grid(a.B + (a.x16 ? (a.n8 + 64 * waves - 1) / (64 * waves) : 0));
   if (a.E <= 64) {
-    if (a.bf16) hipLaunchKernelGGL((route_kernel<true, 1>), dim3(a.B), block, 0, s, a);
-    else hipLaunchKernelGGL((route_kernel<false, 1>), dim3(a.B), block, 0, s, a);
+    if (a.bf16) hipLaunchKernelGGL((route_kernel<true, 1>), grid, block, 0, s, a);
+    else hipLaunchKernelGGL((route_kernel<false, 1>), grid, block, 0, s, a);
   } else if (a.E <= 128) {
-    if (a.bf16) hipLaunchKernelGGL((route_kernel<true, 2>), dim3(a.B), block, 0, s, a);
-    else hipLaunchKernelGGL((route_kernel<false, 2>), dim3(a.B), block, 0, s, a);
+    if (a.bf16) hipLaunchKernelGGL((route_kernel<true, 2>), grid, block, 0, s, a);
+    else hipLaunchKernelGGL((route_kernel<false, 2>), grid, block, 0, s, a);
   } else {
-    if (a.bf16) hipLaunchKernelGGL((route_kernel<true, 4>), dim3(a.B), block, 0, s, a);
-    else hipLaunchKernelGGL((route_kernel<false, 4>), dim3(a.B), block, 0, s, a);
+    if (a.bf16) hipLaunchKernelGGL((route_kernel<true, 4>), grid, block, 0, s, a);
+    else hipLaunchKernelGGL((route_kernel<false, 4>), grid, block, 0, s, a);
   }
   return hipGetLastError();
 }

@@ -9,10 +9,10 @@
   B = 2, too many segments, B = 8, B = 16, fp32 weights).
 * The number of launches, read from a captured HIP graph: 3 on the fused
   path against 6 (bf16) or 7 (int4: x to fp16 is a launch of its own) for
-  the same layer as four calls; one fewer than the four
-  calls where the gating launch ranks the logits itself; the same count
-  where the routing ranks in its own workgroups or the logits are too many
-  to stage.
+  the same layer as four calls; one fewer than the four calls where the
+  gating launch ranks the logits itself; with int4 weights also without the
+  x conversion and the K parts' reduce; the same count where the routing
+  ranks in its own workgroups or the logits are too many to stage.
 * Against the oracle on the fused cases (routing exact, outputs within the
   bf16 tolerance), and graph replays equal to the eager call.
 """
@@ -73,6 +73,9 @@ CASES = [
                                           wdt="q4g32"), 2, False),
     ("B64 E256 (unstaged gate)", _shape(ffn=256, n_experts=256, top_k=4, cap=8, alpha=0.5), 64,
      False),
+    ("int4 B16 K parts", _shape(ffn=8192, cap=4, alpha=0.5, wdt="q4g32"), 16, False),
+    ("int4 B12 E96 K parts rows", _shape(hidden=128, ffn=4096, n_experts=96, cap=4, alpha=0.5,
+                                         wdt="q4g32"), 12, False),
 ]
 
 
@@ -154,9 +157,11 @@ def test_moe_layer_equals_four_calls(label, shape, B, fused, packed):
 # (case, launches of one call, launches of the four calls).  Three on the
 # fused path; elsewhere the gating launch ranks the logits itself where the
 # routing would rank them in a launch of its own (B <= 8 or E > 64, logits
-# staged in LDS or a single-wave gate), and nothing changes otherwise.
+# staged in LDS or a single-wave gate, up to 16 tokens), and with int4
+# weights the routing launch also converts x and the combine launch also
+# adds the down projection's K parts.
 LAUNCHES = [(1, 3, 6), (2, 3, 6), (8, 5, 6), (12, 3, 7), (14, 5, 5), (19, 6, 6), (15, 3, 7),
-            (18, 6, 7)]
+            (18, 5, 7), (20, 5, 7), (21, 5, 8)]
 
 
 @pytest.mark.parametrize("case,n_call,n_four", LAUNCHES, ids=[CASES[c[0]][0] for c in LAUNCHES])
