@@ -23,10 +23,20 @@
 // - A work item is 16 R W rows of one expert (W = 4 waves, R row tiles per
 //   wave) over one of Q contiguous K parts, for all tokens routed to that
 //   expert.  The launch has at most as many workgroups as fit on the GPU at
-//   once, a multiple of the 8 XCDs.  Each XCD takes a contiguous slice of
-//   the activated experts' items and deals it round-robin to its
-//   workgroups.  (Measured on MI355X: dealing equal runs of consecutive
-//   items, or one workgroup per item, was 3-15 % slower.)
+//   once, a multiple of the 8 XCDs, and deals the items (expert-major)
+//   round-robin over all of them, so every XCD gets an equal share of every
+//   expert.  Buckets of different sizes make items of different cost (a
+//   pass over four token tiles costs about twice one over one tile), and a
+//   share of each keeps the XCDs equally loaded.  Measured on MI355X, 24
+//   int4 layers at 64 tokens, where some layers route 60 tokens to one
+//   expert: contiguous per-XCD slices of the items, which keep an expert's
+//   activations in one to three L2s, were 17 % slower per layer with equal
+//   item counts and 6 % slower with equal estimated costs (items run in
+//   discrete rounds of workgroups, so a cost-balanced cut still leaves some
+//   XCDs a round longer); a work counter taken with an atomic add per item
+//   was 20-35 % slower, the adds of all workgroups serialising on one
+//   address; equal runs of consecutive items, or one workgroup per item,
+//   were 3-15 % slower.
 // - The waves of a workgroup stream different rows over the same K range, so
 //   they share the activations: the workgroup stages the tokens' next
 //   super-step in LDS while the current one is decoded (double-buffered, one
@@ -61,9 +71,6 @@ typedef _Float16 half8v __attribute__((ext_vector_type(8)));
 
 constexpr int kW = 4;     // waves per workgroup
 constexpr int kXcds = 8;  // accelerator dies of an MI355X, each with its own L2
-#ifndef S2MOE_Q4_XCD_SLICES
-#define S2MOE_Q4_XCD_SLICES 1
-#endif
 
 __device__ __forceinline__ f32x4 mfma16(half8v a, half8v b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
@@ -591,19 +598,7 @@ __global__ __launch_bounds__(kW * 64, TMAX >= 4 ? S2MOE_Q4_MINWAVES_T4 : 1) void
   const int rows_r = kMode == 0 ? a.F : a.H;
   const int rows_s = kMode == 0 ? a.Fs : a.H;
   const int n_items = (a.S > 0 ? a.S * (rows_s / kRows) : 0) * Q + max(n_act, 0) * (rows_r / kRows) * Q;
-  // Workgroups are dealt to the XCDs round-robin (blockIdx % kXcds), each
-  // XCD with its own L2.  Each XCD takes one contiguous slice of the items
-  // (expert-major), dealt round-robin to its workgroups, so that an expert's
-  // activations are fetched into one or two L2s instead of all of them.
-  // Which XCD runs a workgroup affects only speed, never results.
-#if S2MOE_Q4_XCD_SLICES
-  const int xcd = blockIdx.x % kXcds, lw = blockIdx.x / kXcds, gx = gridDim.x / kXcds;
-  const int i_lo = (int)((long)n_items * xcd / kXcds);
-  const int i_hi = (int)((long)n_items * (xcd + 1) / kXcds);
-  for (int item = i_lo + lw; item < i_hi; item += gx) {
-#else
   for (int item = blockIdx.x; item < n_items; item += gridDim.x) {
-#endif
     Segment seg;
     int rb, q;
     if (!resolve_item(a, kMode, kRows, Q, n_act, item, &seg, &rb, &q)) break;
