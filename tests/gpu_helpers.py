@@ -37,18 +37,19 @@ def make_inputs(shape, B, seed, rho=0.5, router_std=None, alphas=None, layer=0, 
     return d
 
 
-def run_gpu(shape, d, dev_weights=None, packed=False):
+def run_gpu(shape, d, dev_weights=None, packed=False, fused=False):
     """One pass through the C ABI; returns (host results, device weights).
     With packed=True the weights are re-laid by s2moe_pack_weights first and
     the layer carries S2MOE_PACKED_WEIGHTS (dev_weights are then the packed
-    ones)."""
+    ones).  fused=True: the pass is one s2moe_moe_layer call instead of the
+    four calls (route, gate, verify, combine)."""
     import torch
 
     import paper_2608_15018_amd as s2
 
     B = d["x"].shape[0]
     L = s2.make_layer(shape, flags=shape.flags | (s2.PACKED_WEIGHTS if packed else 0))
-    p = s2.VerifyPass(L, B)
+    p = s2.VerifyPass(L, B, fused=fused)
     x = s2.to_device(d["x"])
     router = s2.to_device(d["router"])
     conf = s2.to_device(d["conf_w"])
@@ -59,6 +60,18 @@ def run_gpu(shape, d, dev_weights=None, packed=False):
     p(x, router, conf, dev_weights[1])
     torch.cuda.synchronize()
     return p.results(), dev_weights
+
+
+def assert_same_bits(a: dict, b: dict, label: str = ""):
+    """Every output of two passes equal bit for bit."""
+    assert a.keys() == b.keys(), label
+    for n in a:
+        x, y = np.asarray(a[n]), np.asarray(b[n])
+        if x.dtype.kind == "f":
+            same = x.shape == y.shape and np.array_equal(x.view(np.uint32), y.view(np.uint32))
+        else:
+            same = np.array_equal(x, y)
+        assert same, f"{label}: {n} differs"
 
 
 def rel_err(got, ref) -> float:

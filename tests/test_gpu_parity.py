@@ -12,8 +12,8 @@ import pytest
 
 import oracle
 from synth.configs import WORKLOAD_ID, WORKLOADS, LayerShape
-from tests.gpu_helpers import (TOL_GATE_W, check_outputs, check_routing, log, make_inputs,
-                               rel_err, run_gpu)
+from tests.gpu_helpers import (TOL_GATE_W, assert_same_bits, check_outputs, check_routing, log,
+                               make_inputs, rel_err, run_gpu)
 
 pytestmark = pytest.mark.gpu
 
@@ -35,11 +35,14 @@ def _oracle(shape, d):
 def _full_check(shape, d, label):
     log(f"[parity] {label}: B={d['x'].shape[0]} H={shape.hidden} F={shape.ffn} "
         f"E={shape.n_experts} k={shape.top_k} S={shape.n_shared} wdt={shape.wdt}")
-    got, _ = run_gpu(shape, d)
+    got, dw = run_gpu(shape, d)
     ref = _oracle(shape, d)
     check_routing(got, ref, label)
     errs = check_outputs(got, ref, shape.wdt, label)
-    log(f"[parity] {label}: ok n_uniq={got['n_uniq']} errs={errs}")
+    # The one-call layer (s2moe_moe_layer) on the same inputs and weights.
+    one, _ = run_gpu(shape, d, dw, fused=True)
+    assert_same_bits(one, got, f"{label} one call")
+    log(f"[parity] {label}: ok n_uniq={got['n_uniq']} errs={errs}, one call equal")
     return got, ref
 
 
@@ -502,6 +505,8 @@ def test_full_c3_alpha_sweep():
         ref = _oracle(shape, d)
         check_routing(got, ref, f"c3 alpha={alpha}")
         check_outputs(got, ref, "bf16", f"c3 alpha={alpha}")
+        one, _ = run_gpu(shape, d, dw, fused=True)
+        assert_same_bits(one, got, f"c3 alpha={alpha} one call")
         ratios[alpha] = ref["reuse_ratio"]
     log(f"[parity] c3 reuse ratio by alpha: {ratios}")
     assert ratios[1.0] <= ratios[0.0]
@@ -532,6 +537,8 @@ def test_full_c5_int4_layers(layer):
             dw = weights_to_device(ex, {})
         log(f"[parity] c5 layer={layer} B={B}")
         got, _ = run_gpu(sh, d, dw)
+        one, _ = run_gpu(sh, d, dw, fused=True)
+        assert_same_bits(one, got, f"c5 l={layer} B={B} one call")
         if B == 16:
             packed, _ = run_gpu(sh, d, packed=True)
             assert np.array_equal(packed["expert_out"], got["expert_out"])
