@@ -38,6 +38,9 @@ CASES = {
                         wdt="q4g32"), (64, 4), 0.6, None, False),
     "int4_packed": (LayerShape(hidden=512, ffn=768, n_experts=8, top_k=2, cap=4, alpha=0.5,
                                wdt="q4g32"), (16, 1), 0.6, None, True),
+    # Down projection in two K parts (partial sums in the scratch array).
+    "int4_kparts": (LayerShape(hidden=512, ffn=4096, n_experts=8, top_k=2, cap=4, alpha=0.5,
+                               wdt="q4g32"), (16, 12), 0.6, None, True),
     # Workspace of exactly the scratch size (512 rows of 16384 bf16), then 8 tokens.
     "at_limit": (LayerShape(hidden=256, ffn=16384, n_experts=8, top_k=2, cap=4, alpha=0.5),
                  (256, 8), 0.6, None, False),
