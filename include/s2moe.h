@@ -238,8 +238,10 @@ s2moe_status s2moe_combine(const s2moe_layer *layer, int32_t n_tokens,
    projection with the combine folded in.  Every other batch runs the four
    calls' kernels one after another, except that the gating launch ranks
    the logits itself where the routing would rank them in a launch of its
-   own.  Layer dispatch cost dominates such small batches (a draft step
-   runs one per MoE layer and token).
+   own, and that with Q4G32 weights the routing launch also makes the fp16
+   copy of x and the combine launch also adds the down projection's K parts
+   (two launches fewer than the four calls).  Layer dispatch cost dominates
+   small batches (a draft step runs one per MoE layer and token).
    Workspace, ownership and stream as for s2moe_verify_moe; y as for
    s2moe_combine. */
 s2moe_status s2moe_moe_layer(const s2moe_layer *layer, int32_t n_tokens, const void *x,
