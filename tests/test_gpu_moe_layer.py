@@ -177,11 +177,13 @@ def test_moe_layer_launch_count(case, n_call, n_four):
     assert (n1, n4) == (n_call, n_four)
 
 
-def test_moe_layer_graph_replays():
-    """Replays of a captured fused call, with eager work and
-    synchronisations in between, equal the eager call bit for bit."""
-    shape = CASES[2][1]
-    d = make_inputs(shape, 3, seed=77, rho=0.5)
+@pytest.mark.parametrize("case", [2, 20, 14], ids=[CASES[c][0] for c in (2, 20, 14)])
+def test_moe_layer_graph_replays(case):
+    """Replays of a captured call, with eager work and synchronisations in
+    between, equal the eager call bit for bit: a fused call, an int4 call
+    whose combine launch adds the K parts, and a 16-token bf16 call."""
+    label, shape, B, _fused = CASES[case]
+    d = make_inputs(shape, B, seed=77, rho=0.5)
     p, ins, w, _dev = _run(shape, d, fused=True, packed=True)
     eager = p.results()
     g = torch.cuda.CUDAGraph()
@@ -198,10 +200,10 @@ def test_moe_layer_graph_replays():
         torch.cuda.synchronize()
         g.replay()
         torch.cuda.synchronize()
-        _assert_same(p.results(), eager, f"replay {rep}")
+        _assert_same(p.results(), eager, f"{label} replay {rep}")
         p(*ins, w)
         torch.cuda.synchronize()
-    log("[moe_layer] graph replays equal the eager call")
+    log(f"[moe_layer] {label}: graph replays equal the eager call")
 
 
 def _random_case(rng):
