@@ -843,10 +843,10 @@ hipError_t device_cus(int* cus) {
 }
 
 // Workgroups of one kernel that fit on a compute unit at once, queried once
-// per kernel (the same on every device of one type).
+// per kernel (the same on every device of one type).  `cache` must be the
+// calling kernel's own: every instantiation has the same function type.
 template <class Kern>
-hipError_t resident_per_cu(Kern kern, int* n) {
-  static std::atomic<int> cache{0};
+hipError_t resident_per_cu(Kern kern, std::atomic<int>& cache, int* n) {
   if ((*n = cache.load(std::memory_order_relaxed)) > 0) return hipSuccess;
   hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(n, kern, kW * 64, 0);
   if (e != hipSuccess) return e;
@@ -861,9 +861,10 @@ hipError_t resident_per_cu(Kern kern, int* n) {
 template <int kMode, int TMAX, int R, int D, int A, int C, bool kPacked>
 hipError_t launch_q4(const FfnArgs& a, int Q, hipStream_t s) {
   auto kern = ffn_q4_kernel<kMode, TMAX, R, D, A, C, kPacked>;
+  static std::atomic<int> resident{0};  // this instantiation's workgroups per CU
   int cus = 0, per_cu = 0;
   hipError_t err = device_cus(&cus);
-  if (err == hipSuccess) err = resident_per_cu(kern, &per_cu);
+  if (err == hipSuccess) err = resident_per_cu(kern, resident, &per_cu);
   if (err != hipSuccess) return err;
   constexpr int kRows = 16 * R * kW;
   const int rows_r = kMode == 0 ? a.F : a.H;
