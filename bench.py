@@ -88,7 +88,8 @@ def ffn_source_hash(wdt: str) -> str:
     """sha256 of the code (comments removed) of the sources the expert-FFN
     kernels of this weight format are built from (identifies the kernel a
     traffic measurement belongs to).  Of kernels.h only the FfnArgs
-    definition counts: the rest declares other kernels."""
+    definition counts, and for int4 weights also the K-part count of the
+    down projection (q4_down_parts): the rest declares other kernels."""
     import hashlib
     import re
     h = hashlib.sha256()
@@ -96,8 +97,11 @@ def ffn_source_hash(wdt: str) -> str:
         with open(os.path.join(ROOT, "paper_2608_15018_amd", "csrc", f), "rb") as fh:
             data = fh.read()
         if f == "kernels.h":
-            m = re.search(rb"struct FfnArgs \{.*?\n\};", data, re.S)
-            data = m.group(0) if m else data
+            parts = [rb"struct FfnArgs \{.*?\n\};"]
+            if wdt == "q4g32":
+                parts.append(rb"#ifndef S2MOE_Q4_DOWN_R.*?inline int q4_down_parts\(.*?\n\}")
+            found = [re.search(p, data, re.S) for p in parts]
+            data = b"".join(m.group(0) for m in found) if all(found) else data
         h.update(_code_only(data))
     return h.hexdigest()
 

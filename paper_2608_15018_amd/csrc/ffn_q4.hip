@@ -580,8 +580,17 @@ __device__ __forceinline__ bool resolve_item(const FfnArgs& a, int mode, int row
       if (seg->n < 0 || seg->base < 0 || seg->base + seg->n > a.B * a.k) seg->n = 0;
     }
   }
-  *rb = rem / Q;
-  *q = rem % Q;
+  // Items are dealt round-robin over the grid (a multiple of kXcds
+  // workgroups), so positions p and p + kXcds of a segment's items run on
+  // the same XCD.  With K parts, the positions p = x (mod kXcds) take the
+  // x-th of kXcds contiguous chunks of the segment's items in (part, row
+  // block) order: each XCD's L2 then holds the activations of at most two of
+  // the segment's Q parts, for any Q <= kXcds.
+  const int per = seg->shared ? per_s : per_r;
+  const int nrb = per / Q;
+  const int L = (Q > 1 && per % kXcds == 0) ? (rem % kXcds) * (per / kXcds) + rem / kXcds : rem;
+  *q = L / nrb;
+  *rb = L % nrb;
   return true;
 }
 

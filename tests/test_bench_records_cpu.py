@@ -56,3 +56,20 @@ def test_oracle_timing_repeats_until_the_time_or_the_cap(monkeypatch):
     import time
     reps, dt = bench.time_oracle(lambda: time.sleep(0.03))
     assert 2 <= reps <= 3 and dt >= 0.05
+
+
+def test_int4_hash_covers_the_down_part_count(tmp_path, monkeypatch):
+    # The K-part count of the int4 down projection sets how many partial sums
+    # are written and read back, so it belongs to the int4 traffic record;
+    # the bf16 kernels do not use it.
+    import shutil
+    src = tmp_path / "paper_2608_15018_amd" / "csrc"
+    shutil.copytree(bench.os.path.join(bench.ROOT, "paper_2608_15018_amd", "csrc"), src)
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    before = {w: bench.ffn_source_hash(w) for w in ("q4g32", "bf16")}
+    kh = src / "kernels.h"
+    text = kh.read_text()
+    assert "0.02 * down / part" in text
+    kh.write_text(text.replace("0.02 * down / part", "0.05 * down / part"))
+    assert bench.ffn_source_hash("q4g32") != before["q4g32"]
+    assert bench.ffn_source_hash("bf16") == before["bf16"]
