@@ -180,8 +180,8 @@ s2moe_status s2moe_verify_moe(const s2moe_layer *layer, int32_t n_tokens, const 
    computed by the same kernels.  A layer and n_tokens whose
    s2moe_workspace_bytes exceed S2MOE_NOALLOC_SCRATCH_BYTES are rejected
    with S2MOE_EUNSUPPORTED before anything is enqueued (c2- to c5-shaped
-   layers at up to 64 tokens need at most about 10 MiB: the int4 layer at 64
-   tokens, with its down projection's partial sums over 4 K parts).  All calls on one
+   layers at up to 64 tokens need at most 8 MiB: the int4 layer at 64
+   tokens, with its down projection's partial sums over 3 K parts).  All calls on one
    GPU share its array: calls that can overlap on the device (different
    streams without ordering, several host threads) race and give undefined
    results.  Calls ordered on one stream are safe; the array's contents

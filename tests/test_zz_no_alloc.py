@@ -38,7 +38,8 @@ CASES = {
                         wdt="q4g32"), (64, 4), 0.6, None, False),
     "int4_packed": (LayerShape(hidden=512, ffn=768, n_experts=8, top_k=2, cap=4, alpha=0.5,
                                wdt="q4g32"), (16, 1), 0.6, None, True),
-    # Down projection in two K parts (partial sums in the scratch array).
+    # Down projection in K parts, 3 at 16 tokens and 4 at 12 (partial sums in
+    # the scratch array; 12 and 16 down items per expert).
     "int4_kparts": (LayerShape(hidden=512, ffn=4096, n_experts=8, top_k=2, cap=4, alpha=0.5,
                                wdt="q4g32"), (16, 12), 0.6, None, True),
     # Workspace of exactly the scratch size (512 rows of 16384 bf16), then 8 tokens.
