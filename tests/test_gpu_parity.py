@@ -276,6 +276,28 @@ def test_max_hidden():
         _full_check(shape, d, f"H=16384 B={B}")
 
 
+@pytest.mark.parametrize("wdt", ["bf16", "q4g32"])
+def test_max_ffn(wdt):
+    """F = 262144 (the documented maximum): 4096 gate-up row blocks per
+    expert and a down projection over 2048 super-steps of K; with int4
+    weights the down launch splits K into its largest count of parts (8)."""
+    shape = LayerShape(hidden=128, ffn=262144, n_experts=2, top_k=1, cap=1, alpha=0.5, wdt=wdt)
+    d = make_inputs(shape, 12, seed=41, rho=0.5)
+    _full_check(shape, d, f"F=262144 {wdt}")
+
+
+@pytest.mark.parametrize("wdt", ["bf16", "q4g32"])
+def test_max_shared_experts(wdt):
+    """S = 8 shared experts (the ABI maximum) beside 16 routed ones, with
+    F_s > F, so Hh rows are F_s wide and expert_out holds rows B k + s B + b
+    for every s."""
+    shape = LayerShape(hidden=256, ffn=256, n_experts=16, top_k=2, n_shared=8, ffn_shared=384,
+                       cap=4, alpha=0.5, wdt=wdt)
+    d = make_inputs(shape, 20, seed=31, rho=0.5)
+    got, _ = _full_check(shape, d, f"S=8 {wdt}")
+    assert got["expert_out"].shape[0] == 20 * 2 + 8 * 20
+
+
 def test_cap_equal_E_and_identical_tokens():
     shape = LayerShape(hidden=256, ffn=256, n_experts=16, top_k=3, cap=16, alpha=0.9)
     d = make_inputs(shape, 12, seed=5, rho=0.5)
