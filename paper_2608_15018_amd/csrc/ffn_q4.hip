@@ -25,7 +25,10 @@
 //   expert.  The launch has at most as many workgroups as fit on the GPU at
 //   once, a multiple of the 8 XCDs, and deals the items (expert-major)
 //   round-robin over all of them, so every XCD gets an equal share of every
-//   expert.  Buckets of different sizes make items of different cost (a
+//   expert.  Within an expert, the down items one XCD receives form one
+//   contiguous run of its (part, row block) list (resolve_item), so that
+//   XCD's L2 fetches the activations of at most two of the Q parts.  Buckets
+//   of different sizes make items of different cost (a
 //   pass over four token tiles costs about twice one over one tile), and a
 //   share of each keeps the XCDs equally loaded.  Measured on MI355X, 24
 //   int4 layers at 64 tokens, where some layers route 60 tokens to one
@@ -35,7 +38,8 @@
 //   discrete rounds of workgroups, so a cost-balanced cut still leaves some
 //   XCDs a round longer); a work counter taken with an atomic add per item
 //   was 20-35 % slower, the adds of all workgroups serialising on one
-//   address; equal runs of consecutive items, or one workgroup per item,
+//   address, and claims on 8 counters past the first round of items 1-2 %
+//   slower; equal runs of consecutive items, or one workgroup per item,
 //   were 3-15 % slower.
 // - The waves of a workgroup stream different rows over the same K range, so
 //   they share the activations: the workgroup stages the tokens' next
