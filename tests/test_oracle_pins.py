@@ -32,7 +32,7 @@ def brute_topk(values, k):
 
 
 # ---------------------------------------------------------------- route (a1, a2)
-def test_router_one_hot_rows_pick_coordinates():
+def check_router_orientation(O_mod):
     """W_r with unit rows e_{p(e)} gives ell_{b,e} = x_{b,p(e)}: pins the
     orientation ell = W_r x (a transposed router changes which coordinate is
     read)."""
@@ -42,26 +42,33 @@ def test_router_one_hot_rows_pick_coordinates():
     perm = np.array([3, 11, 0, 7, 15, 2])
     W = np.zeros((E, H), np.float32)
     W[np.arange(E), perm] = 1.0
-    r = oracle.route(x, W, 2, "f32")
+    r = O_mod.route(x, W, 2, "f32")
     np.testing.assert_array_equal(r["logits"], x[:, perm].astype(np.float64))
 
 
-def test_router_matches_explicit_loop_on_bf16_bits():
+def test_router_one_hot_rows_pick_coordinates():
+    check_router_orientation(O)
+
+
+def check_router_bf16(O_mod):
     """Logits on bf16 inputs equal the dot products of the decoded values;
     decoded values are checked against known bf16 encodings."""
     known = {0x3F80: 1.0, 0xC000: -2.0, 0x3F81: 1.0078125, 0x0000: 0.0,
              0x4049: 3.140625, 0xBF00: -0.5}
     for bits, val in known.items():
-        assert oracle.upcast(np.array([bits], np.uint16), "bf16")[0] == val
+        assert O_mod.upcast(np.array([bits], np.uint16), "bf16")[0] == val
     x = np.array([[0x3F80, 0xC000, 0x4049]], np.uint16)     # [1, -2, 3.140625]
     W = np.array([[0x3F80, 0x3F80, 0x0000],                 # [1, 1, 0]
                   [0x0000, 0xBF00, 0x3F80]], np.uint16)     # [0, -0.5, 1]
-    r = oracle.route(x, W, 1, "bf16")
+    r = O_mod.route(x, W, 1, "bf16")
     np.testing.assert_array_equal(r["logits"], [[-1.0, 1.0 + 3.140625]])
 
 
-@pytest.mark.parametrize("seed", range(20))
-def test_plain_topk_and_gap_bruteforce(seed):
+def test_router_matches_explicit_loop_on_bf16_bits():
+    check_router_bf16(O)
+
+
+def check_plain_topk_and_gap(O_mod, seed):
     rng = np.random.default_rng(seed)
     E = int(rng.integers(3, 9))
     k = int(rng.integers(1, min(4, E)))
@@ -69,7 +76,7 @@ def test_plain_topk_and_gap_bruteforce(seed):
     H = 8
     x = rng.standard_normal((B, H))
     W = rng.standard_normal((E, H))
-    r = oracle.route(x.astype(np.float32), W.astype(np.float32), k, "f32")
+    r = O_mod.route(x.astype(np.float32), W.astype(np.float32), k, "f32")
     for b in range(B):
         ell = list(r["logits"][b])
         assert list(r["plain_idx"][b]) == brute_topk(ell, k)
@@ -77,11 +84,20 @@ def test_plain_topk_and_gap_bruteforce(seed):
         assert r["gap"][b] == desc[0] - desc[k]          # top-1 minus (k+1)-th
 
 
-def test_ties_break_toward_lower_expert_index():
+@pytest.mark.parametrize("seed", range(20))
+def test_plain_topk_and_gap_bruteforce(seed):
+    check_plain_topk_and_gap(O, seed)
+
+
+def check_ties(O_mod):
     ell = np.array([[1.0, 2.0, 2.0, 0.5, 2.0]])
-    r_idx = O.top_k_ascending(ell[0], 2)
+    r_idx = O_mod.top_k_ascending(ell[0], 2)
     assert list(r_idx) == [1, 2]
-    assert list(O.rank_order(np.array([0.0, -0.0, 0.0]))) == [0, 1, 2]
+    assert list(O_mod.rank_order(np.array([0.0, -0.0, 0.0]))) == [0, 1, 2]
+
+
+def test_ties_break_toward_lower_expert_index():
+    check_ties(O)
 
 
 # ---------------------------------------------------------------- gating (a3-a5)
@@ -228,14 +244,14 @@ def test_gate_weights_are_softmax_of_original_logits():
                                    rtol=1e-14, atol=0)
 
 
-def test_bucketing_matches_stable_argsort():
+def check_bucketing(O_mod):
     rng = np.random.default_rng(3)
     for _ in range(20):
         E = int(rng.integers(2, 20))
         k = int(rng.integers(1, min(E, 5)))
         B = int(rng.integers(1, 40))
         idx = np.array([np.sort(rng.choice(E, k, replace=False)) for _ in range(B)])
-        bk = oracle.bucket(idx, E)
+        bk = O_mod.bucket(idx, E)
         flat = idx.reshape(-1)
         np.testing.assert_array_equal(bk["slot"], np.argsort(flat, kind="stable"))
         np.testing.assert_array_equal(bk["count"], np.bincount(flat, minlength=E))
@@ -247,8 +263,23 @@ def test_bucketing_matches_stable_argsort():
         assert bk["reuse_ratio"] == u.size / (B * k)
 
 
+def test_bucketing_matches_stable_argsort():
+    check_bucketing(O)
+
+
+def check_route_and_bucket_pins(O_mod):
+    """Every pin of the router, the plain top-k with its gap, the tie rule
+    and the bucketing, run on one oracle module."""
+    check_router_orientation(O_mod)
+    check_router_bf16(O_mod)
+    for seed in range(20):
+        check_plain_topk_and_gap(O_mod, seed)
+    check_ties(O_mod)
+    check_bucketing(O_mod)
+
+
 # ---------------------------------------------------------------- FFN (a7-a11)
-def test_swiglu_closed_form_identity_weights():
+def check_swiglu_identity(O_mod):
     """W_g = c I, W_u = I, W_d = P (a permutation): y = P (silu(c x) * x).
     Swapping gate and up gives silu(x) * c x, a transposed W_d gives P^T."""
     rng = np.random.default_rng(11)
@@ -260,29 +291,36 @@ def test_swiglu_closed_form_identity_weights():
                "up": np.eye(H)[None].astype(np.float32),
                "down": P[None].astype(np.float32)}
     gt = {"idx": np.zeros((3, 1), np.int32)}
-    out = oracle.verify_moe(x, experts, {}, gt, 1, "f32", "f32")
+    out = O_mod.verify_moe(x, experts, {}, gt, 1, "f32", "f32")
     xd = x.astype(np.float64)
     expect = (c * xd * expit(c * xd) * xd) @ P.T
     np.testing.assert_allclose(out, expect, rtol=1e-14, atol=1e-15)
 
 
-def test_down_projection_is_linear_and_zero_gives_zero():
+def test_swiglu_closed_form_identity_weights():
+    check_swiglu_identity(O)
+
+
+def check_down_linear(O_mod):
     rng = np.random.default_rng(12)
     H, F, E = 8, 16, 3
     x = rng.standard_normal((4, H)).astype(np.float32)
     ex = {n: rng.standard_normal((E, F, H)).astype(np.float32) for n in ("gate", "up")}
     ex["down"] = rng.standard_normal((E, H, F)).astype(np.float32)
     gt = {"idx": np.array([[0, 2], [1, 2], [0, 1], [2, 0]], np.int32)}
-    base = oracle.verify_moe(x, ex, {}, gt, 2, "f32", "f32")
+    base = O_mod.verify_moe(x, ex, {}, gt, 2, "f32", "f32")
     ex2 = dict(ex, down=ex["down"] * np.float32(2.0))
-    np.testing.assert_allclose(oracle.verify_moe(x, ex2, {}, gt, 2, "f32", "f32"), 2 * base,
+    np.testing.assert_allclose(O_mod.verify_moe(x, ex2, {}, gt, 2, "f32", "f32"), 2 * base,
                                rtol=1e-14)
     ex0 = dict(ex, down=np.zeros_like(ex["down"]))
-    assert not oracle.verify_moe(x, ex0, {}, gt, 2, "f32", "f32").any()
+    assert not O_mod.verify_moe(x, ex0, {}, gt, 2, "f32", "f32").any()
 
 
-@pytest.mark.parametrize("seed", range(8))
-def test_dense_then_mask_bruteforce(seed):
+def test_down_projection_is_linear_and_zero_gives_zero():
+    check_down_linear(O)
+
+
+def check_dense_then_mask(O_mod, seed):
     """All experts on all tokens, then a one-hot gate mask (einsum-based)
     equals the oracle's grouped verify_moe + combine."""
     rng = np.random.default_rng(200 + seed)
@@ -298,8 +336,8 @@ def test_dense_then_mask_bruteforce(seed):
     idx = np.array([np.sort(rng.choice(E, k, replace=False)) for _ in range(B)], np.int32)
     gw = rng.random((B, k))
     gw /= gw.sum(1, keepdims=True)
-    eo = oracle.verify_moe(x, ex, sh, {"idx": idx}, k, "f32", "f32", S)
-    y = oracle.combine(gw, eo, k, S)
+    eo = O_mod.verify_moe(x, ex, sh, {"idx": idx}, k, "f32", "f32", S)
+    y = O_mod.combine(gw, eo, k, S)
 
     X = x.astype(np.float64)
     a = np.einsum("bh,efh->bef", X, ex["gate"].astype(np.float64))
@@ -315,7 +353,12 @@ def test_dense_then_mask_bruteforce(seed):
     np.testing.assert_allclose(y, ref, rtol=1e-12, atol=1e-12)
 
 
-def test_int4_dequant_known_codes():
+@pytest.mark.parametrize("seed", range(8))
+def test_dense_then_mask_bruteforce(seed):
+    check_dense_then_mask(O, seed)
+
+
+def check_int4_known_codes(O_mod):
     """Byte 0x8F holds element 0 = 15 (low nibble) and element 1 = 8 (high);
     with scale 0.5: w = 0.5 * (15 - 8) = 3.5 and 0.5 * (8 - 8) = 0."""
     codes = np.zeros((2, 32), np.uint8)          # rows=2, K=64 -> 2 groups per row
@@ -323,7 +366,7 @@ def test_int4_dequant_known_codes():
     codes[0, 16] = 0x10                          # group 1: elem 32 = 0, elem 33 = 1
     codes[1, :] = 0x88                           # all exactly zero
     scales = np.array([[0.5, 0.25], [3.0, 7.0]], np.float16)
-    w = oracle.dequant_q4g32(codes, scales)
+    w = O_mod.dequant_q4g32(codes, scales)
     assert w.shape == (2, 64)
     assert w[0, 0] == 3.5 and w[0, 1] == 0.0
     assert w[0, 2] == 0.5 * (0 - 8)
@@ -331,8 +374,12 @@ def test_int4_dequant_known_codes():
     assert not w[1].any()
 
 
+def test_int4_dequant_known_codes():
+    check_int4_known_codes(O)
+
+
 # ---------------------------------------------------------------- combine (a10)
-def test_combine_small_numbers():
+def check_combine_small(O_mod):
     eo = np.array([[1.0, 2.0],     # token 0, slot 0
                    [10.0, 20.0],   # token 0, slot 1
                    [3.0, 4.0],     # token 1, slot 0
@@ -340,9 +387,24 @@ def test_combine_small_numbers():
                    [100.0, 0.0],   # shared 0, token 0
                    [0.0, 100.0]])  # shared 0, token 1
     gw = np.array([[0.25, 0.75], [0.5, 0.5]])
-    y = oracle.combine(gw, eo, 2, 1)
+    y = O_mod.combine(gw, eo, 2, 1)
     np.testing.assert_array_equal(y, [[0.25 + 7.5 + 100.0, 0.5 + 15.0],
                                       [1.5 + 15.0, 2.0 + 20.0 + 100.0]])
+
+
+def test_combine_small_numbers():
+    check_combine_small(O)
+
+
+def check_ffn_pins(O_mod):
+    """Every pin of the expert FFN, dequantisation and combine steps, run on
+    one oracle module (the oracle itself, or a copy with a planted mistake)."""
+    check_swiglu_identity(O_mod)
+    check_down_linear(O_mod)
+    for seed in range(8):
+        check_dense_then_mask(O_mod, seed)
+    check_int4_known_codes(O_mod)
+    check_combine_small(O_mod)
 
 
 # ---------------------------------------------------------------- reuse ratio
