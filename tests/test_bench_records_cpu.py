@@ -73,3 +73,28 @@ def test_int4_hash_covers_the_down_part_count(tmp_path, monkeypatch):
     kh.write_text(text.replace("0.02 * down / part", "0.05 * down / part"))
     assert bench.ffn_source_hash("q4g32") != before["q4g32"]
     assert bench.ffn_source_hash("bf16") == before["bf16"]
+
+
+def test_committed_traffic_records_match_the_kernel_sources():
+    """Each committed HBM-traffic summary was taken with the kernel sources as
+    they are now: bench.py reports its traffic only then, so a kernel change
+    must come with new counter runs."""
+    import glob
+    import os
+    import re
+    recs = sorted(glob.glob(os.path.join(bench.ROOT, "profiles", "*_traffic.md")))
+    assert recs, "no traffic records under profiles/"
+    wdt_of = {"c2": "bf16", "c3": "bf16", "c4": "bf16", "c5": "q4g32"}
+    stale = []
+    for path in recs:
+        name = os.path.basename(path)
+        m = re.search(r"kernel_source_sha256: `([0-9a-f]{64})`", open(path).read())
+        assert m, f"{name}: no kernel_source_sha256 line"
+        if name.startswith("expand_"):
+            want = bench.expand_source_hash()
+        else:
+            wl = re.match(r"verify_moe_(c\d)", name).group(1)
+            want = bench.ffn_source_hash(wdt_of[wl])
+        if m.group(1) != want:
+            stale.append(name)
+    assert not stale, f"traffic records taken with other kernel sources: {stale}"
