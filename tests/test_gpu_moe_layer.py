@@ -128,11 +128,15 @@ def _graph_kernel_nodes(fn) -> int:
     return int(n.value)
 
 
-@pytest.mark.parametrize("packed", [False, True])
-@pytest.mark.parametrize("label,shape,B,fused", CASES, ids=[c[0] for c in CASES])
-def test_moe_layer_equals_four_calls(label, shape, B, fused, packed):
-    if packed and shape.wdt == "f32":
-        pytest.skip("fp32 weights are not packed")
+# Every case with row-major weights, and again packed where the weights can be
+# (the packed layout exists for bf16 and int4 weights only).
+LAYOUTS = [(c, False) for c in CASES] + [(c, True) for c in CASES if c[1].wdt != "f32"]
+
+
+@pytest.mark.parametrize("case,packed", LAYOUTS,
+                         ids=[f"{c[0]}-{'packed' if p else 'rows'}" for c, p in LAYOUTS])
+def test_moe_layer_equals_four_calls(case, packed):
+    label, shape, B, fused = case
     d = make_inputs(shape, B, seed=31 + B + shape.n_experts, rho=0.5)
     tag = f"{label} packed={packed}"
     log(f"[moe_layer] {tag}: H={shape.hidden} F={shape.ffn} E={shape.n_experts} "
