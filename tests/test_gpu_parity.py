@@ -543,12 +543,14 @@ def test_full_c4_shared_routed():
 @pytest.mark.parametrize("layer", [0, 11, 23])
 def test_full_c5_int4_layers(layer):
     """Mixtral-shaped int4 layers 0, 11 and 23 of the 24-layer stack, each at
-    draft sizes 1, 4, 16 and 64.  The oracle uses the exact fp32 values of
-    the dequantised weights (s * (q - 8) has at most 15 significant bits)."""
+    draft sizes 1, 4, 16, 32 and 64 (every kernel configuration: the K-split
+    kernel, then one, two and four token tiles per weight pass with 4, 4 and
+    3 K parts of the down projection).  The oracle uses the exact fp32 values
+    of the dequantised weights (s * (q - 8) has at most 15 significant bits)."""
     wl = WORKLOADS["c5"]
     sh = wl.shape
     dw = deq = None
-    for B in (1, 4, 16, 64):
+    for B in (1, 4, 16, 32, 64):
         d = _workload_inputs("c5", B, seed=1, layer=layer)
         if dw is None:
             from paper_2608_15018_amd.pipeline import weights_to_device
@@ -561,7 +563,7 @@ def test_full_c5_int4_layers(layer):
         got, _ = run_gpu(sh, d, dw)
         one, _ = run_gpu(sh, d, dw, fused=True)
         assert_same_bits(one, got, f"c5 l={layer} B={B} one call")
-        if B == 16:
+        if B in (16, 64):
             packed, _ = run_gpu(sh, d, packed=True)
             assert np.array_equal(packed["expert_out"], got["expert_out"])
         ref = oracle.forward(d["x"], d["router"], d["conf_w"], deq, {}, sh.with_(wdt="f32"))
