@@ -119,6 +119,24 @@ def test_workspace_size_and_errors(lib):
     assert lib.s2moe_workspace_bytes(ctypes.byref(_layer(cap=0)), 4) == 0
 
 
+def test_int4_workspace_holds_the_down_k_parts(lib):
+    """With int4 weights the workspace holds Hh, the fp16 copy of x and the
+    fp32 partial sums of the down projection's K parts 1 .. Q-1.  At the
+    Mixtral shape the part rule (at least 1024 down items of 128 rows, at
+    most 8 parts, the partial sums within 2 % of the down weights' bytes, one
+    part at up to 8 tokens) gives Q = 1, 1, 4, 4 and 3 at 1, 4, 16, 32 and 64
+    tokens."""
+    H, F, E, k = 4096, 14336, 8, 2
+    L = _layer(hidden=H, ffn=F, n_experts=E, top_k=k, cap=4, wdt="q4g32")
+    r256 = lambda n: (n + 255) // 256 * 256  # noqa: E731
+    down_bytes = E * F * H * (0.5 + 2 / 32)
+    for B, Q in ((1, 1), (4, 1), (16, 4), (32, 4), (64, 3)):
+        rows = B * k
+        part = (Q - 1) * rows * H * 4
+        assert part <= 0.02 * down_bytes
+        assert s2.workspace_bytes(L, B) == r256(rows * F * 2) + r256(B * H * 2) + r256(part), B
+
+
 def test_binding_raises_with_message():
     with pytest.raises(s2.S2moeError) as ei:
         s2.workspace_bytes(_layer(top_k=0), 4)
