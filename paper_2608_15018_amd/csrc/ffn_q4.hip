@@ -60,6 +60,7 @@
 //   workspace, and q4_reduce_kernel adds them in part order afterwards, so
 //   the result does not depend on timing.
 #include <atomic>
+#include <type_traits>
 
 #include "q4_layout.h"
 #include "small_layer.h"
@@ -651,19 +652,33 @@ __global__ __launch_bounds__(kW * 64, TMAX >= 4 ? S2MOE_Q4_MINWAVES_T4 : 1) void
   }
 }
 
+// Element quad i of expert_out plus the partial sums of K parts 1 .. Q - 1
+// (part q at part[(q - 1) n4 + i]), added in part order.  The Q loads are all
+// issued before the first addition, so a quad costs one memory round trip.
+template <int Q>
+__device__ __forceinline__ f32x4 q4_sum_parts(const f32x4* out, const f32x4* part, size_t n4,
+                                              size_t i) {
+  f32x4 p[Q];
+  p[0] = out[i];
+#pragma unroll
+  for (int q = 1; q < Q; ++q) p[q] = part[(size_t)(q - 1) * n4 + i];
+  f32x4 v = p[0];
+#pragma unroll
+  for (int q = 1; q < Q; ++q)
+#pragma unroll
+    for (int c = 0; c < 4; ++c) v[c] += p[q][c];
+  return v;
+}
+
 // expert_out += the partial sums of K parts 1 .. Q - 1, added in part order.
+template <int Q>
 __global__ __launch_bounds__(256) void q4_reduce_kernel(float* __restrict__ out,
-                                                        const float* __restrict__ part, int Q,
+                                                        const float* __restrict__ part,
                                                         size_t n4) {
   const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= n4) return;
-  f32x4 v = reinterpret_cast<const f32x4*>(out)[i];
-  for (int q = 1; q < Q; ++q) {
-    const f32x4 p = reinterpret_cast<const f32x4*>(part)[(size_t)(q - 1) * n4 + i];
-#pragma unroll
-    for (int c = 0; c < 4; ++c) v[c] += p[c];
-  }
-  reinterpret_cast<f32x4*>(out)[i] = v;
+  reinterpret_cast<f32x4*>(out)[i] = q4_sum_parts<Q>(reinterpret_cast<const f32x4*>(out),
+                                                     reinterpret_cast<const f32x4*>(part), n4, i);
 }
 
 // The ordered reduce and the combine in one launch (the one-call layer): for
@@ -671,6 +686,7 @@ __global__ __launch_bounds__(256) void q4_reduce_kernel(float* __restrict__ out,
 // then the shared rows B k + s B + b) gets parts 1 .. Q - 1 added in part
 // order and goes back to expert_out, as q4_reduce_kernel does; y is then
 // formed from those rows with combine_kernel's arithmetic.
+template <int Q>
 __global__ __launch_bounds__(256) void q4_reduce_combine_kernel(FfnArgs a, CombineArgs c) {
   const int b = blockIdx.y;
   const int col = blockIdx.x * blockDim.x + threadIdx.x;
@@ -681,12 +697,7 @@ __global__ __launch_bounds__(256) void q4_reduce_combine_kernel(FfnArgs a, Combi
   const f32x4* part = reinterpret_cast<const f32x4*>(a.part);
   auto reduce_row = [&](int r) {
     const size_t i = (size_t)r * ldq + col;
-    f32x4 v = out[i];
-    for (int q = 1; q < a.qparts; ++q) {
-      const f32x4 p = part[(size_t)(q - 1) * n4 + i];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) v[e] += p[e];
-    }
+    const f32x4 v = q4_sum_parts<Q>(out, part, n4, i);
     out[i] = v;
     return v;
   };
@@ -1027,10 +1038,28 @@ hipError_t launch_moe_layer_small_q4(const RouteArgs& ra, const GateArgs& ga, co
                   : launch_q4_small_layer<false>(ra, ga, a, y, s);
 }
 
-hipError_t launch_q4_reduce_combine(const FfnArgs& a, const CombineArgs& c, hipStream_t s) {
-  hipLaunchKernelGGL(q4_reduce_combine_kernel, dim3((a.H / 4 + 255) / 256, a.B), dim3(256), 0, s,
-                     a, c);
+// Calls f with std::integral_constant<int, Q> for a launch's part count
+// Q = 2 .. 8 (q4_down_parts returns at most 8), then checks the launch.
+template <class F>
+hipError_t with_q4_parts(int Q, F&& f) {
+  switch (Q) {
+    case 2: f(std::integral_constant<int, 2>()); break;
+    case 3: f(std::integral_constant<int, 3>()); break;
+    case 4: f(std::integral_constant<int, 4>()); break;
+    case 5: f(std::integral_constant<int, 5>()); break;
+    case 6: f(std::integral_constant<int, 6>()); break;
+    case 7: f(std::integral_constant<int, 7>()); break;
+    case 8: f(std::integral_constant<int, 8>()); break;
+    default: return hipErrorInvalidValue;
+  }
   return hipGetLastError();
+}
+
+hipError_t launch_q4_reduce_combine(const FfnArgs& a, const CombineArgs& c, hipStream_t s) {
+  const dim3 grid((a.H / 4 + 255) / 256, a.B);
+  return with_q4_parts(a.qparts, [&](auto q) {
+    hipLaunchKernelGGL((q4_reduce_combine_kernel<decltype(q)::value>), grid, dim3(256), 0, s, a, c);
+  });
 }
 
 hipError_t launch_ffn_q4(const FfnArgs& a, hipStream_t s) {
@@ -1049,9 +1078,11 @@ hipError_t launch_ffn_q4(const FfnArgs& a, hipStream_t s) {
   else err = launch_q4_pair<S2MOE_Q4_TMAX_LARGE>(a, s);
   if (err != hipSuccess || a.qparts <= 1 || a.defer_reduce) return err;
   const size_t n4 = ((size_t)a.B * a.k + (size_t)a.S * a.B) * a.H / 4;
-  hipLaunchKernelGGL(q4_reduce_kernel, dim3((unsigned)((n4 + 255) / 256)), dim3(256), 0, s, a.out,
-                     a.part, a.qparts, n4);
-  return hipGetLastError();
+  const dim3 grid((unsigned)((n4 + 255) / 256));
+  return with_q4_parts(a.qparts, [&](auto q) {
+    hipLaunchKernelGGL((q4_reduce_kernel<decltype(q)::value>), grid, dim3(256), 0, s, a.out,
+                       static_cast<const float*>(a.part), n4);
+  });
 }
 
 }  // namespace s2moe
